@@ -1,0 +1,154 @@
+"""ctypes front end of the fp64 CPU oracle (oracle/transx_oracle.c).
+
+TEST INFRASTRUCTURE ONLY: imported by tests/, by the package smoke check and by
+the benchmark's CPU-baseline leg, never by the product path.
+
+`build()` compiles the C source with gcc; `Oracle` holds one model's weights
+as float64 and exposes the oracle's stages (full encode, incremental append,
+cross-attention K/V, decoder + head).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "transx_oracle.c")
+_LIB = os.path.join(_HERE, "libtransx_oracle.so")
+
+
+def build(verbose: bool = False, src: str = _SRC, out: str = _LIB) -> str:
+    """Compile the oracle (plain C, fp64, OpenMP). Always recompiles."""
+    tmp = out + ".tmp"
+    cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-ffp-contract=off",
+           "-o", tmp, src, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, out)
+    return out
+
+
+class _Cfg(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int), ("H", ctypes.c_int), ("F", ctypes.c_int), ("n_enc", ctypes.c_int),
+                ("n_dec", ctypes.c_int), ("R", ctypes.c_int), ("eps", ctypes.c_double)]
+
+
+_libs = {}
+
+
+def _load(path: Optional[str] = None):
+    path = path or _LIB
+    if path not in _libs:
+        if path == _LIB and not os.path.exists(_LIB):
+            build()
+        lib = ctypes.CDLL(path)
+        P = ctypes.POINTER
+        dp = P(ctypes.c_double)
+        wp = P(dp)
+        lib.ox_n_weights.argtypes = [P(_Cfg)]
+        lib.ox_n_weights.restype = ctypes.c_int
+        lib.ox_encode.argtypes = [P(_Cfg), wp, dp, ctypes.c_int, dp, dp, dp, dp]
+        lib.ox_encode_append.argtypes = [P(_Cfg), wp, dp, dp, ctypes.c_int, dp, ctypes.c_int, dp, dp, dp]
+        lib.ox_cross_kv.argtypes = [P(_Cfg), wp, dp, ctypes.c_int, dp, dp]
+        lib.ox_score.argtypes = [P(_Cfg), wp, dp, dp, ctypes.c_int, dp, ctypes.c_int, dp, ctypes.c_int, dp, dp, dp]
+        for f in ("ox_encode", "ox_encode_append", "ox_cross_kv", "ox_score"):
+            getattr(lib, f).restype = None
+        _libs[path] = lib
+    return _libs[path]
+
+
+def _dp(a: Optional[np.ndarray]):
+    if a is None:
+        return ctypes.POINTER(ctypes.c_double)()
+    assert a.dtype == np.float64 and a.flags.c_contiguous
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+
+
+class Oracle:
+    """One model (config + weights in canonical order) evaluated in fp64."""
+
+    def __init__(self, model, weights: Sequence[np.ndarray], lib_path: Optional[str] = None):
+        self.model = model
+        self.lib = _load(lib_path)
+        self.cfg = _Cfg(model.d_model, model.n_heads, model.d_ffn, model.n_enc_layers, model.n_dec_layers,
+                        model.rel_pos_buckets, float(model.ln_eps))
+        n = self.lib.ox_n_weights(ctypes.byref(self.cfg))
+        if n != len(weights):
+            raise ValueError(f"oracle expects {n} tensors, got {len(weights)}")
+        self._w = [_f64(w).reshape(-1) if np.asarray(w).size else np.zeros(1) for w in weights]
+        self._wp = (ctypes.POINTER(ctypes.c_double) * n)(*[_dp(w) for w in self._w])
+
+    @property
+    def d(self) -> int:
+        return self.model.d_model
+
+    def encode(self, X) -> Tuple[np.ndarray, np.ndarray, np.ndarray, float]:
+        """Full causal encoding of [L, d] tokens -> (H_enc [L,d], K_enc, V_enc
+        [n_enc, L, d], max |softmax row sum - 1|)."""
+        X = _f64(X)
+        L = X.shape[0]
+        H = np.empty((L, self.d))
+        K = np.empty((self.model.n_enc_layers, L, self.d))
+        V = np.empty_like(K)
+        err = np.zeros(1)
+        self.lib.ox_encode(ctypes.byref(self.cfg), self._wp, _dp(X), L, _dp(H), _dp(K), _dp(V), _dp(err))
+        return H, K, V, float(err[0])
+
+    def encode_append(self, Kpre, Vpre, Xnew) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+        """Encode n new tokens after a cached prefix given its per-layer K/V
+        [n_enc, len, d] -> (H_new [n,d], K_new, V_new [n_enc, n, d])."""
+        Kpre, Vpre, Xnew = _f64(Kpre), _f64(Vpre), _f64(Xnew)
+        ln, n = Kpre.shape[1], Xnew.shape[0]
+        H = np.empty((n, self.d))
+        K = np.empty((self.model.n_enc_layers, n, self.d))
+        V = np.empty_like(K)
+        self.lib.ox_encode_append(ctypes.byref(self.cfg), self._wp, _dp(Kpre), _dp(Vpre), ln, _dp(Xnew), n, _dp(H),
+                                  _dp(K), _dp(V))
+        return H, K, V
+
+    def cross_kv(self, Henc) -> Tuple[np.ndarray, np.ndarray]:
+        """Cross-attention K/V of every decoder layer: [n_dec, L, d] each."""
+        Henc = _f64(Henc)
+        L = Henc.shape[0]
+        K = np.empty((self.model.n_dec_layers, L, self.d))
+        V = np.empty_like(K)
+        self.lib.ox_cross_kv(ctypes.byref(self.cfg), self._wp, _dp(Henc), L, _dp(K), _dp(V))
+        return K, V
+
+    def score(self, Kx, Vx, Xs, Xc, trace: bool = False):
+        """Decoder + head. Returns scores [C] (and, with trace=True, also the
+        per-layer sublayer outputs [n_dec, 3, S+C, d] and the max softmax
+        row-sum deviation)."""
+        Kx, Vx, Xs, Xc = _f64(Kx), _f64(Vx), _f64(Xs), _f64(Xc)
+        L = Kx.shape[1]
+        S, C = Xs.shape[0], Xc.shape[0]
+        out = np.empty(C)
+        tr = np.empty((self.model.n_dec_layers, 3, S + C, self.d)) if trace else None
+        err = np.zeros(1)
+        self.lib.ox_score(ctypes.byref(self.cfg), self._wp, _dp(Kx), _dp(Vx), L, _dp(Xs), S, _dp(Xc), C, _dp(out),
+                          _dp(tr), _dp(err))
+        if trace:
+            return out, tr, float(err[0])
+        return out
+
+    def run_request(self, Xb, Xs, Xc, Xev=None):
+        """Whole path for one request: encode behavior (then append events if
+        given), project cross K/V, decode, score. Returns (scores, state dict)."""
+        H, K, V, _ = self.encode(Xb)
+        if Xev is not None and len(Xev):
+            Hn, Kn, Vn = self.encode_append(K, V, Xev)
+            H = np.concatenate([H, Hn], 0)
+            K = np.concatenate([K, Kn], 1)
+            V = np.concatenate([V, Vn], 1)
+        Kx, Vx = self.cross_kv(H)
+        s = self.score(Kx, Vx, Xs, Xc)
+        return s, {"H": H, "K": K, "V": V, "Kx": Kx, "Vx": Vx}

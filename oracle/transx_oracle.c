@@ -1,0 +1,344 @@
+/*
+ * transx_oracle.c -- plain fp64 CPU oracle of the TransX amortized serving path.
+ *
+ * TEST INFRASTRUCTURE ONLY. Nothing on the product path may link, load or call
+ * this file; only the tests, the package smoke check and the benchmark's CPU
+ * baseline use it. It shares no code, header or table with the HIP library.
+ *
+ * What it computes (TransX, arXiv 2607.28940):
+ *   - behavior encoder: causal Transformer blocks, self-attention + FFN with
+ *     residual connections and post-LayerNorm (Sec. 4.1.1), with a learned
+ *     per-head relative-position bias on the attention logits (Sec. 4.1.1 and
+ *     App. D, remark on incremental encoding; Table encoder-ablation "rel pos
+ *     bias"),
+ *   - cached cross-attention keys/values K = Phi_b W_K, V = Phi_b W_V shared by
+ *     every query of the request (Sec. 4.1.2, multi-query cross-attention),
+ *   - decoder layers over [serving tokens; candidate tokens]: self-attention
+ *     with the candidate-isolating mask (App. B, Transformer head), dense
+ *     cross-attention softmax(Q K^T / sqrt(d_h)) V over all cached tokens
+ *     (Sec. 4.1.2, Eq. sparse-cross-attn with the index set = all tokens),
+ *     the crossAttend residual/LayerNorm block (Sec. 4.1.2) and an FFN,
+ *   - a linear scalar head on the candidate rows (the k = 2 case of Sec. 4.1.3,
+ *     Eq. action-decoding),
+ *   - incremental append: only the new tokens are encoded, against the stored
+ *     per-layer keys/values of the prefix (App. D, remark on incremental
+ *     encoding; Sec. 4.2, causal attention and prefix reuse).
+ *
+ * Readings where the paper is silent or ambiguous:
+ *   - decoder sublayer order self -> cross -> FFN, separate softmaxes,
+ *   - the FFN residual is taken from the attention sublayer's output
+ *     (standard post-LN block) rather than from the block input,
+ *   - LayerNorm: biased variance, eps from the config, learned gain/offset,
+ *   - GELU: exact erf form,
+ *   - relative bias beta_h[min(i - j, R - 1)] added to encoder logits, R = 0
+ *     disables it; the decoder has no position term,
+ *   - every projection has a bias; y = x W with W stored [d_in, d_out]; head h
+ *     owns columns h*d_h .. h*d_h + d_h - 1.
+ *
+ * Everything is double precision, evaluated in the order the definitions
+ * state. OpenMP only splits independent rows / (head, query) pairs.
+ */
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+typedef struct {
+  int d;       /* model width */
+  int H;       /* heads */
+  int F;       /* FFN hidden width */
+  int n_enc;   /* encoder layers */
+  int n_dec;   /* decoder layers */
+  int R;       /* relative-position buckets, 0 = no bias */
+  double eps;  /* LayerNorm epsilon */
+} ox_cfg;
+
+/* Parameter list, canonical order (see paper_2607_28940_amd/inputs.py):
+ * per encoder layer 17 tensors, per decoder layer 26, then the head (2). */
+enum { E_WQ, E_BQ, E_WK, E_BK, E_WV, E_BV, E_WO, E_BO, E_LN1G, E_LN1B,
+       E_W1, E_B1, E_W2, E_B2, E_LN2G, E_LN2B, E_REL, E_COUNT };
+enum { D_SWQ, D_SBQ, D_SWK, D_SBK, D_SWV, D_SBV, D_SWO, D_SBO, D_LN1G, D_LN1B,
+       D_XWQ, D_XBQ, D_XWK, D_XBK, D_XWV, D_XBV, D_XWO, D_XBO, D_LN2G, D_LN2B,
+       D_W1, D_B1, D_W2, D_B2, D_LN3G, D_LN3B, D_COUNT };
+
+static const double* encw(const ox_cfg* c, const double* const* W, int e, int k) {
+  (void)c;
+  return W[e * E_COUNT + k];
+}
+static const double* decw(const ox_cfg* c, const double* const* W, int l, int k) {
+  return W[c->n_enc * E_COUNT + l * D_COUNT + k];
+}
+static const double* headw(const ox_cfg* c, const double* const* W, int k) {
+  return W[c->n_enc * E_COUNT + c->n_dec * D_COUNT + k];
+}
+
+int ox_n_weights(const ox_cfg* c) { return c->n_enc * E_COUNT + c->n_dec * D_COUNT + 2; }
+
+/* ---------------------------------------------------------------- building blocks */
+
+/* Y[M][N] = X[M][K] W[K][N] + b[N]  (a linear layer, y = x W + b) */
+static void linear(const double* X, int M, int K, const double* W, const double* b, int N, double* Y) {
+#pragma omp parallel for schedule(static)
+  for (int i = 0; i < M; ++i) {
+    double* y = Y + (size_t)i * N;
+    for (int j = 0; j < N; ++j) y[j] = 0.0;
+    for (int k = 0; k < K; ++k) {
+      const double x = X[(size_t)i * K + k];
+      const double* w = W + (size_t)k * N;
+      for (int j = 0; j < N; ++j) y[j] += x * w[j];
+    }
+    for (int j = 0; j < N; ++j) y[j] += b[j];
+  }
+}
+
+/* Y[i] = LN(A[i] + B[i]) over the d features of each row (post-LN residual). */
+static void add_layernorm(const double* A, const double* B, int M, int d, const double* g,
+                          const double* beta, double eps, double* Y) {
+#pragma omp parallel for schedule(static)
+  for (int i = 0; i < M; ++i) {
+    double mean = 0.0, var = 0.0;
+    for (int j = 0; j < d; ++j) mean += A[(size_t)i * d + j] + B[(size_t)i * d + j];
+    mean /= d;
+    for (int j = 0; j < d; ++j) {
+      const double t = A[(size_t)i * d + j] + B[(size_t)i * d + j] - mean;
+      var += t * t;
+    }
+    var /= d;
+    const double inv = 1.0 / sqrt(var + eps);
+    for (int j = 0; j < d; ++j) {
+      const double t = A[(size_t)i * d + j] + B[(size_t)i * d + j];
+      Y[(size_t)i * d + j] = (t - mean) * inv * g[j] + beta[j];
+    }
+  }
+}
+
+static double gelu(double x) { return 0.5 * x * (1.0 + erf(x / sqrt(2.0))); }
+
+enum { MASK_NONE = 0, MASK_CAUSAL = 1, MASK_SERVING_CANDIDATE = 2 };
+
+/*
+ * Multi-head scaled dot-product attention, softmax(q k^T / sqrt(d_h) + bias) v
+ * per head (Sec. 4.1.2, Eq. sparse-cross-attn), on row-major Q [nq][ldq],
+ * K [nk][ldk], V [nk][ldv]; head h uses columns h*dh .. h*dh+dh-1. Output
+ * O [nq][d].
+ *
+ * mask MASK_NONE: every query sees every key (cross-attention over the cache).
+ * mask MASK_CAUSAL: query i sits at position qpos0 + i and sees keys j <= that
+ *   position; the logit gets rel[h][min(pos - j, R - 1)] when R > 0 (encoder).
+ * mask MASK_SERVING_CANDIDATE: rows i < S (serving tokens) see keys j <= i;
+ *   rows i >= S (candidates) see keys j < S and j == i (App. B mask).
+ * If rowsum_err is given, the largest |sum_j p_ij - 1| is folded into it.
+ */
+static void attention(int nq, int nk, int d, int H, const double* Q, int ldq, const double* K, int ldk,
+                      const double* V, int ldv, int mask, int qpos0, int S, const double* rel, int R,
+                      double* O, double* rowsum_err) {
+  const int dh = d / H;
+  const double scale = 1.0 / sqrt((double)dh);
+  double worst = 0.0;
+#pragma omp parallel for schedule(dynamic, 4) reduction(max : worst)
+  for (int t = 0; t < nq * H; ++t) {
+    const int i = t / H, h = t % H;
+    double* logit = (double*)malloc(sizeof(double) * (size_t)(nk > 0 ? nk : 1));
+    unsigned char* seen = (unsigned char*)malloc((size_t)(nk > 0 ? nk : 1));
+    double mx = -INFINITY;
+    for (int j = 0; j < nk; ++j) {
+      int ok = 1;
+      if (mask == MASK_CAUSAL) ok = j <= qpos0 + i;
+      else if (mask == MASK_SERVING_CANDIDATE) ok = (i < S) ? (j <= i) : (j < S || j == i);
+      seen[j] = (unsigned char)ok;
+      if (!ok) continue;
+      double s = 0.0;
+      for (int k = 0; k < dh; ++k) s += Q[(size_t)i * ldq + h * dh + k] * K[(size_t)j * ldk + h * dh + k];
+      s *= scale;
+      if (mask == MASK_CAUSAL && R > 0) {
+        int dist = qpos0 + i - j;
+        if (dist > R - 1) dist = R - 1;
+        s += rel[h * R + dist];
+      }
+      logit[j] = s;
+      if (s > mx) mx = s;
+    }
+    double den = 0.0;
+    for (int j = 0; j < nk; ++j)
+      if (seen[j]) den += exp(logit[j] - mx);
+    double psum = 0.0;
+    double* o = O + (size_t)i * d + h * dh;
+    for (int k = 0; k < dh; ++k) o[k] = 0.0;
+    for (int j = 0; j < nk; ++j) {
+      if (!seen[j]) continue;
+      const double p = exp(logit[j] - mx) / den;
+      psum += p;
+      for (int k = 0; k < dh; ++k) o[k] += p * V[(size_t)j * ldv + h * dh + k];
+    }
+    if (fabs(psum - 1.0) > worst) worst = fabs(psum - 1.0);
+    free(logit);
+    free(seen);
+  }
+  if (rowsum_err && worst > *rowsum_err) *rowsum_err = worst;
+}
+
+/* FFN sublayer with post-LN: Y = LN(X + GELU(X W1 + b1) W2 + b2). */
+static void ffn_block(const ox_cfg* c, const double* X, int M, const double* W1, const double* b1,
+                      const double* W2, const double* b2, const double* g, const double* beta, double* Y) {
+  double* h = (double*)malloc(sizeof(double) * (size_t)M * c->F);
+  double* f = (double*)malloc(sizeof(double) * (size_t)M * c->d);
+  linear(X, M, c->d, W1, b1, c->F, h);
+  for (size_t k = 0; k < (size_t)M * c->F; ++k) h[k] = gelu(h[k]);
+  linear(h, M, c->F, W2, b2, c->d, f);
+  add_layernorm(X, f, M, c->d, g, beta, c->eps, Y);
+  free(h);
+  free(f);
+}
+
+/* ---------------------------------------------------------------- encoder */
+
+/*
+ * One causal encoder layer over rows whose positions are pos0 .. pos0+n-1,
+ * attending to the stored prefix keys/values (positions 0 .. pos0-1) and to
+ * themselves (Sec. 4.1.1; App. D remark on incremental encoding).
+ *   X      [n][d]      layer input of the new rows, replaced by the layer output
+ *   Kall   [pos0+n][d] prefix keys on entry (rows < pos0); rows pos0.. are written
+ *   Vall   [pos0+n][d] same for values
+ */
+static void encoder_layer(const ox_cfg* c, const double* const* W, int e, double* X, int n, int pos0,
+                          double* Kall, double* Vall, double* rowsum_err) {
+  const int d = c->d;
+  double* Q = (double*)malloc(sizeof(double) * (size_t)n * d);
+  double* A = (double*)malloc(sizeof(double) * (size_t)n * d);
+  double* P = (double*)malloc(sizeof(double) * (size_t)n * d);
+  double* Y = (double*)malloc(sizeof(double) * (size_t)n * d);
+  linear(X, n, d, encw(c, W, e, E_WQ), encw(c, W, e, E_BQ), d, Q);
+  linear(X, n, d, encw(c, W, e, E_WK), encw(c, W, e, E_BK), d, Kall + (size_t)pos0 * d);
+  linear(X, n, d, encw(c, W, e, E_WV), encw(c, W, e, E_BV), d, Vall + (size_t)pos0 * d);
+  attention(n, pos0 + n, d, c->H, Q, d, Kall, d, Vall, d, MASK_CAUSAL, pos0, 0, encw(c, W, e, E_REL), c->R, A,
+            rowsum_err);
+  linear(A, n, d, encw(c, W, e, E_WO), encw(c, W, e, E_BO), d, P);
+  add_layernorm(X, P, n, d, encw(c, W, e, E_LN1G), encw(c, W, e, E_LN1B), c->eps, Y);
+  ffn_block(c, Y, n, encw(c, W, e, E_W1), encw(c, W, e, E_B1), encw(c, W, e, E_W2), encw(c, W, e, E_B2),
+            encw(c, W, e, E_LN2G), encw(c, W, e, E_LN2B), X);
+  free(Q);
+  free(A);
+  free(P);
+  free(Y);
+}
+
+/*
+ * Full encoding of a behavior sequence (Sec. 4.2, the whole stream is encoded
+ * once, left to right).
+ *   X    [L][d]            behavior tokens
+ *   Henc [L][d]            encoder output Phi_behavior(H)
+ *   Kenc, Venc [n_enc][L][d]  each layer's self-attention keys and values
+ */
+void ox_encode(const ox_cfg* c, const double* const* W, const double* X, int L, double* Henc, double* Kenc,
+               double* Venc, double* rowsum_err) {
+  memcpy(Henc, X, sizeof(double) * (size_t)L * c->d);
+  for (int e = 0; e < c->n_enc; ++e)
+    encoder_layer(c, W, e, Henc, L, 0, Kenc + (size_t)e * L * c->d, Venc + (size_t)e * L * c->d, rowsum_err);
+}
+
+/*
+ * Incremental encoding of n new behavior tokens appended after len cached
+ * ones (App. D remark: with a causal encoder and relative position bias the
+ * cached tokens' states do not change; only the new tokens are computed).
+ *   Kpre, Vpre [n_enc][len][d]  stored per-layer keys/values of the prefix
+ *   Xnew [n][d]                 new tokens
+ *   Hnew [n][d]                 encoder output of the new tokens
+ *   Knew, Vnew [n_enc][n][d]    per-layer keys/values of the new tokens
+ */
+void ox_encode_append(const ox_cfg* c, const double* const* W, const double* Kpre, const double* Vpre, int len,
+                      const double* Xnew, int n, double* Hnew, double* Knew, double* Vnew) {
+  const int d = c->d;
+  double* Kall = (double*)malloc(sizeof(double) * (size_t)(len + n) * d);
+  double* Vall = (double*)malloc(sizeof(double) * (size_t)(len + n) * d);
+  memcpy(Hnew, Xnew, sizeof(double) * (size_t)n * d);
+  for (int e = 0; e < c->n_enc; ++e) {
+    memcpy(Kall, Kpre + (size_t)e * len * d, sizeof(double) * (size_t)len * d);
+    memcpy(Vall, Vpre + (size_t)e * len * d, sizeof(double) * (size_t)len * d);
+    encoder_layer(c, W, e, Hnew, n, len, Kall, Vall, NULL);
+    memcpy(Knew + (size_t)e * n * d, Kall + (size_t)len * d, sizeof(double) * (size_t)n * d);
+    memcpy(Vnew + (size_t)e * n * d, Vall + (size_t)len * d, sizeof(double) * (size_t)n * d);
+  }
+  free(Kall);
+  free(Vall);
+}
+
+/*
+ * Cross-attention keys and values of every decoder layer, computed once per
+ * request from the encoder output and shared by all its queries
+ * (Sec. 4.1.2, K = Phi_b W_K, V = Phi_b W_V; Sec. 4.3, KV caching).
+ *   Henc [L][d] -> Kx, Vx [n_dec][L][d]
+ */
+void ox_cross_kv(const ox_cfg* c, const double* const* W, const double* Henc, int L, double* Kx, double* Vx) {
+  for (int l = 0; l < c->n_dec; ++l) {
+    linear(Henc, L, c->d, decw(c, W, l, D_XWK), decw(c, W, l, D_XBK), c->d, Kx + (size_t)l * L * c->d);
+    linear(Henc, L, c->d, decw(c, W, l, D_XWV), decw(c, W, l, D_XBV), c->d, Vx + (size_t)l * L * c->d);
+  }
+}
+
+/*
+ * Decoder and scoring head for one request.
+ *   Kx, Vx [n_dec][L][d]   cached cross-attention keys/values
+ *   Xs [S][d]              serving-event tokens (causal among themselves)
+ *   Xc [C][d]              candidate tokens (see all serving tokens and
+ *                          themselves, not each other: App. B mask)
+ *   scores [C]             s_c = z_c . w_s + b_s, the candidate logit
+ *   trace (optional)       [n_dec][3][S+C][d]: rows after the self-attention,
+ *                          cross-attention and FFN sublayers of each layer
+ *   rowsum_err (optional)  max |sum p - 1| over every softmax row
+ * Layer: T1 = LN(T + SelfAttn(T) W_o + b_o); T2 = LN(T1 + CrossAttn(T1) W_o^x
+ * + b_o^x); T = LN(T2 + FFN(T2)) (Sec. 4.1.2, crossAttend block, with the
+ * candidate self-attention of App. B before it).
+ */
+void ox_score(const ox_cfg* c, const double* const* W, const double* Kx, const double* Vx, int L,
+              const double* Xs, int S, const double* Xc, int C, double* scores, double* trace,
+              double* rowsum_err) {
+  const int d = c->d, N = S + C;
+  double* T = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1) * d);
+  double* Q = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1) * d);
+  double* K = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1) * d);
+  double* V = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1) * d);
+  double* A = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1) * d);
+  double* P = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1) * d);
+  double* T1 = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1) * d);
+  double* T2 = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1) * d);
+  memcpy(T, Xs, sizeof(double) * (size_t)S * d);
+  memcpy(T + (size_t)S * d, Xc, sizeof(double) * (size_t)C * d);
+  for (int l = 0; l < c->n_dec; ++l) {
+    /* self-attention among serving tokens and candidates */
+    linear(T, N, d, decw(c, W, l, D_SWQ), decw(c, W, l, D_SBQ), d, Q);
+    linear(T, N, d, decw(c, W, l, D_SWK), decw(c, W, l, D_SBK), d, K);
+    linear(T, N, d, decw(c, W, l, D_SWV), decw(c, W, l, D_SBV), d, V);
+    attention(N, N, d, c->H, Q, d, K, d, V, d, MASK_SERVING_CANDIDATE, 0, S, NULL, 0, A, rowsum_err);
+    linear(A, N, d, decw(c, W, l, D_SWO), decw(c, W, l, D_SBO), d, P);
+    add_layernorm(T, P, N, d, decw(c, W, l, D_LN1G), decw(c, W, l, D_LN1B), c->eps, T1);
+    /* cross-attention onto the cached behavior keys/values */
+    linear(T1, N, d, decw(c, W, l, D_XWQ), decw(c, W, l, D_XBQ), d, Q);
+    attention(N, L, d, c->H, Q, d, Kx + (size_t)l * L * d, d, Vx + (size_t)l * L * d, d, MASK_NONE, 0, 0, NULL, 0,
+              A, rowsum_err);
+    linear(A, N, d, decw(c, W, l, D_XWO), decw(c, W, l, D_XBO), d, P);
+    add_layernorm(T1, P, N, d, decw(c, W, l, D_LN2G), decw(c, W, l, D_LN2B), c->eps, T2);
+    /* FFN */
+    ffn_block(c, T2, N, decw(c, W, l, D_W1), decw(c, W, l, D_B1), decw(c, W, l, D_W2), decw(c, W, l, D_B2),
+              decw(c, W, l, D_LN3G), decw(c, W, l, D_LN3B), T);
+    if (trace) {
+      double* tr = trace + (size_t)l * 3 * N * d;
+      memcpy(tr, T1, sizeof(double) * (size_t)N * d);
+      memcpy(tr + (size_t)N * d, T2, sizeof(double) * (size_t)N * d);
+      memcpy(tr + (size_t)2 * N * d, T, sizeof(double) * (size_t)N * d);
+    }
+  }
+  const double* ws = headw(c, W, 0);
+  const double bs = headw(c, W, 1)[0];
+  for (int j = 0; j < C; ++j) {
+    double s = 0.0;
+    for (int k = 0; k < d; ++k) s += T[(size_t)(S + j) * d + k] * ws[k];
+    scores[j] = s + bs;
+  }
+  free(T);
+  free(Q);
+  free(K);
+  free(V);
+  free(A);
+  free(P);
+  free(T1);
+  free(T2);
+}
