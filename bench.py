@@ -1,0 +1,218 @@
+#!/usr/bin/env python3
+"""Throughput of TransX candidate scoring on one MI355X.
+
+One step = one score_candidates call over the whole batch: every request's
+serving-event tokens and candidates run through the decoder (self-attention,
+cross-attention onto the request's cached behavior K/V, FFN) and the linear
+head. The caches are built (untimed) before the timed region; inputs are
+resident in HBM when it starts. Prints one JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload headline]
+
+The JSON carries the roofline of the dominant kernel, whose per-launch time
+comes from HIP events the library records around each launch on the stream
+(tx_profile_*), and the fp64 CPU oracle's own throughput on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+METRIC = "candidate scores/sec + % bf16 MFMA peak, B=256 L=4096 C=512 on 1 MI355X"
+
+
+def score_work(wl):
+    """Algorithmic flops and bytes of one score call: the contractions the
+    decoder must do once the cache exists (QKV/O/cross-Q/cross-O/FFN GEMMs,
+    self- and cross-attention, head) and the bytes it must move (cached K/V
+    read once, tokens in, scores out, weights once). In the last decoder layer
+    serving rows only supply their self-attention keys and values."""
+    m = wl.model
+    d, F = m.d_model, m.d_ffn
+    es = 2 if m.dtype == "bf16" else 4
+    f_gemm = f_cross = f_self = 0.0
+    for L, S, C in zip(wl.L, wl.S, wl.C):
+        N = S + C
+        for layer in range(m.n_dec_layers):
+            last = layer == m.n_dec_layers - 1
+            rows = C if last else N
+            f_gemm += (12 * d * d + 4 * d * F) * rows + (4 * d * d * S if last else 0)
+            f_cross += 4.0 * L * d * rows
+            f_self += (0 if last else 2.0 * d * S * (S + 1)) + 4.0 * d * C * (S + 1)
+        f_gemm += 2 * d * C
+    kv = sum(m.n_dec_layers * 2 * L * d for L in wl.L) * es
+    tok = sum(S + C for S, C in zip(wl.S, wl.C)) * d * es
+    wts = m.n_dec_layers * (12 * d * d + 2 * d * F) * es
+    return {"flop": f_gemm + f_cross + f_self, "flop_gemm": f_gemm, "flop_cross": f_cross, "flop_self": f_self,
+            "bytes": float(kv + tok + 4 * sum(wl.C) + wts), "bytes_kv": float(kv)}
+
+
+def cpu_baseline(wl, weights, n_req: int):
+    """The fp64 oracle's score phase on the first n_req requests, wall clock on
+    the host's cores. Its cross-attention cache is seeded N(0,1) data of the
+    right shape (the phase's cost does not depend on the values)."""
+    import numpy as np
+    from oracle import oracle as O
+    from paper_2607_28940_amd import inputs as I
+    O.build()
+    orc = O.Oracle(wl.model, weights)
+    m = wl.model
+    n_scores = 0
+    elapsed = 0.0
+    for r in range(n_req):
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([I.SEED_X, wl.cfg_id, 7, r])))
+        Kx = rng.standard_normal((m.n_dec_layers, wl.L[r], m.d_model))
+        Vx = rng.standard_normal((m.n_dec_layers, wl.L[r], m.d_model))
+        Xs = I.request_tokens(wl, r, I.STREAM_SERVING)
+        Xc = I.request_tokens(wl, r, I.STREAM_CANDIDATES)
+        t0 = time.perf_counter()
+        orc.score(Kx, Vx, Xs, Xc)
+        elapsed += time.perf_counter() - t0
+        n_scores += len(Xc)
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": n_scores / elapsed, "unit": "scores/s", "cores": cores, "kind": "oracle",
+            "sample": f"score phase of the fp64 oracle on {n_req} request(s) of the workload "
+                      f"({n_scores} scores, {elapsed:.1f} s), cache contents seeded N(0,1)"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="headline", choices=["headline", "uniform", "ragged", "tiny"])
+    ap.add_argument("--cpu-requests", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true", help="time without per-launch events")
+    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="HBM bytes per launch from rocprofv3 counters (optional)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the serving path shards by request with no exchange between GPUs, "
+              "and this build runs on a single MI355X. Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2607_28940_amd import inputs as I
+    from paper_2607_28940_amd import transx as T
+
+    assert torch.cuda.is_available(), "bench.py needs a ROCm GPU"
+    torch.cuda.set_device(0)
+    wl = I.workload(args.workload)
+    m = wl.model
+    t_setup = time.time()
+    weights = I.make_weights(m)
+    model = T.Model(m, weights)
+    n_pages = sum((L + 63) // 64 for L in wl.L)
+    cache = T.KVCache(model, n_pages=n_pages, max_requests=wl.B, max_tokens=max(wl.L))
+    # build every request's cache (untimed), a few requests at a time
+    chunk = max(1, (1 << 19) // max(1, max(wl.L)))
+    for a in range(0, wl.B, chunk):
+        ids = list(range(a, min(wl.B, a + chunk)))
+        Xb = T.to_device(I.packed_tokens(wl, I.STREAM_BEHAVIOR, ids, threads=16), m)
+        cache.build(ids, Xb, I.offsets([wl.L[r] for r in ids]), ws_limit=8 << 30)
+        del Xb
+    xs = T.to_device(I.packed_tokens(wl, I.STREAM_SERVING, threads=16), m)
+    xc = T.to_device(I.packed_tokens(wl, I.STREAM_CANDIDATES, threads=16), m)
+    so, co = I.offsets(wl.S), I.offsets(wl.C)
+    ids = list(range(wl.B))
+    out = torch.empty(int(co[-1]), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    print(f"# setup {time.time() - t_setup:.1f} s: {wl.B} caches built", file=sys.stderr, flush=True)
+
+    for _ in range(args.warmup):
+        cache.score(ids, xs, so, xc, co, out=out)
+    torch.cuda.synchronize()
+    if not args.no_profile:
+        T.profile_enable(True)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        cache.score(ids, xs, so, xc, co, out=out)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    prof = {}
+    if not args.no_profile:
+        prof = T.profile_read()
+        T.profile_enable(False)
+    assert bool(torch.isfinite(out).all()), "non-finite scores"
+
+    work = score_work(wl)
+    n_scores = int(co[-1])
+    value = n_scores / (ms / 1e3)
+    tflops = work["flop"] / (ms / 1e3) / 1e12
+    peak = PEAK_BF16_TFLOPS if m.dtype == "bf16" else PEAK_FP32_TFLOPS
+
+    kernels = {}
+    for name, p in prof.items():
+        avg = p["ms"] / p["launches"]
+        kernels[name] = {"avg_ms": round(avg, 5), "launches_per_step": p["launches"] / args.steps,
+                         "share": round(p["ms"] / (ms * args.steps), 4),
+                         "tflops": round(p["flops"] / (p["ms"] / 1e3) / 1e12, 2) if p["flops"] else None,
+                         "gbs": round(p["bytes"] / (p["ms"] / 1e3) / 1e9, 1)}
+    roofline = None
+    if prof:
+        dom = max(prof, key=lambda k: prof[k]["ms"])
+        p = prof[dom]
+        avg_s = p["ms"] / p["launches"] / 1e3
+        fl_launch, by_launch = p["flops"] / p["launches"], p["bytes"] / p["launches"]
+        mfma = fl_launch > 0 and fl_launch / max(by_launch, 1) > peak * 1e12 / (PEAK_HBM_GBS * 1e9)
+        traffic = None
+        if os.path.exists(args.traffic_json):
+            try:
+                traffic = json.load(open(args.traffic_json)).get(dom)
+            except (OSError, ValueError):
+                traffic = None
+        if mfma:
+            ach = fl_launch / avg_s / 1e12
+            roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
+                        "frac": round(ach / peak, 4), "traffic": traffic,
+                        "per_launch": {"flop": fl_launch, "bytes": by_launch, "avg_ms": round(avg_s * 1e3, 5)}}
+        else:
+            ach = by_launch / avg_s / 1e9
+            roofline = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+                        "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": traffic,
+                        "per_launch": {"flop": fl_launch, "bytes": by_launch, "avg_ms": round(avg_s * 1e3, 5)}}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, weights, min(args.cpu_requests, wl.B))
+
+    line = {
+        "metric": METRIC if args.workload == "headline" else f"candidate scores/sec, {args.workload} on 1 MI355X",
+        "value": round(value, 1), "unit": "scores/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": m.dtype, "data": "synthetic (seeded N(0,1) tokens, N(0,0.02) weights)",
+        "config": {"workload": f"{args.workload}: B={wl.B} L={'ragged' if len(set(wl.L)) > 1 else wl.L[0]} "
+                               f"S={'ragged' if len(set(wl.S)) > 1 else wl.S[0]} "
+                               f"C={'ragged' if len(set(wl.C)) > 1 else wl.C[0]} d={m.d_model} H={m.n_heads} "
+                               f"F={m.d_ffn} n_enc={m.n_enc_layers} n_dec={m.n_dec_layers} page=64",
+                   "global_batch": wl.B, "scores_per_step": n_scores},
+        "mfma_frac_of_peak": round(tflops / peak, 4),
+        "achieved_tflops": round(tflops, 2),
+        "algorithmic": {"flop_per_step": work["flop"], "bytes_per_step": work["bytes"]},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,436 @@
+// Attention kernels of the TransX path.
+//
+// paged attention  softmax(q k^T / sqrt(d_h) [+ rel bias]) v with keys/values
+//                  read from the request's cache pages. Serves the decoder
+//                  cross-attention (every query of a request sees every cached
+//                  token: Sec. 4.1.2, Eq. sparse-cross-attn with the index set
+//                  = all tokens, K/V shared by all the request's queries) and the
+//                  causal encoder (queries at positions pos0+i see positions
+//                  <= their own, logit + beta_h[min(i - j, R - 1)]: Sec. 4.1.1,
+//                  App. D remark on incremental encoding).
+// self-attention   decoder self-attention with the candidate-isolating mask
+//                  (App. B): serving tokens causal among themselves, candidate
+//                  c sees every serving token and itself.
+//
+// Softmax is the online (running max / running sum) form in fp32 in the base-2
+// domain: logits are scaled by log2(e) and exponentiated with exp2.
+#include "tx_internal.h"
+
+namespace tx {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// ============================================================================
+// bf16 paged attention on MFMA.
+//
+// A block of 4 waves serves up to 128 queries of one (request, head); each
+// wave owns 32 queries. For every 64-token page the block stages K [64][dh]
+// and V^T [dh][64] in LDS (double-buffered, the next page prefetched into
+// registers while the current one is used), so every K/V byte fetched from
+// HBM/L2 feeds all queries of the block.
+//
+// Per wave and page:  S^T = K Q^T  (v_mfma_f32_32x32x16_bf16, keys as rows so
+// that a lane holds 32 keys of one query: the softmax row reduction is within
+// the lane plus one exchange with lane l^32), online softmax update, then
+// O^T += V^T P^T with P^T taken straight from the S^T accumulators (the MFMA
+// k index is permuted consistently on both operands, so no register shuffle
+// is needed; V^T supplies the matching keys with two 8-byte LDS reads).
+// Keys past the request's length are masked by selection and their V columns
+// are zeroed in LDS so that unused page slots (of any content) never reach
+// the output.
+// ============================================================================
+template <int DH, bool CAUSAL>
+__global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict__ q, int ldq, bf16* __restrict__ out,
+                                                           int ldo, const bf16* __restrict__ pool,
+                                                           const int32_t* __restrict__ page_table, int max_pages,
+                                                           PageGeom g, int layer_slot, const AttnReq* __restrict__ reqs,
+                                                           const AttnTile* __restrict__ tiles,
+                                                           const float* __restrict__ rel, int R, float scale_log2) {
+  constexpr int KLD = DH + 8;  // LDS row stride of K (elements)
+  constexpr int VLD = 64 + 8;  // LDS row stride of V^T
+  constexpr int NCH = 64 * DH / 8 / 256;  // 16-byte chunks per thread per slab
+  __shared__ __attribute__((aligned(16))) bf16 sK[2][64 * KLD];
+  __shared__ __attribute__((aligned(16))) bf16 sV[2][DH * VLD];
+
+  const AttnTile tile = tiles[blockIdx.x];
+  if (tile.q_count <= 0) return;
+  const AttnReq rq = reqs[tile.req];
+  const int h = tile.head;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, hi = lane >> 5;
+
+  const int qi = wave * 32 + l32;
+  const bool wave_active = wave * 32 < tile.q_count;
+  const bool q_valid = qi < tile.q_count;
+  const int i = tile.q_begin + min(qi, tile.q_count - 1);
+  const int row = i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
+  const int qpos = rq.pos0 + i;
+
+  // Q as the MFMA B operand: lane holds Q[query l32][16*kk + 8*hi .. +8]
+  bf16x8 qf[DH / 16];
+  {
+    const bf16* qr = q + (size_t)row * ldq + h * DH + 8 * hi;
+#pragma unroll
+    for (int kk = 0; kk < DH / 16; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qr + 16 * kk);
+  }
+
+  floatx16 o[DH / 32];
+#pragma unroll
+  for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const int kv_len = rq.kv_len;
+  int n_pages = (kv_len + kPage - 1) / kPage;
+  if (CAUSAL) {
+    const int last_pos = rq.pos0 + tile.q_begin + tile.q_count - 1;
+    n_pages = min(n_pages, last_pos / kPage + 1);
+  }
+  const int32_t* ptab = page_table + (size_t)rq.slot * max_pages;
+
+  bf16x8 rk[NCH], rv[NCH];
+  auto gload = [&](int p) {
+    const size_t base = (size_t)ptab[p] * g.page_elems;
+    const bf16x8* kp = reinterpret_cast<const bf16x8*>(pool + base + g.k_off(layer_slot, h));
+    const bf16x8* vp = reinterpret_cast<const bf16x8*>(pool + base + g.v_off(layer_slot, h));
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      rk[u] = kp[tid + 256 * u];
+      rv[u] = vp[tid + 256 * u];
+    }
+  };
+  auto lstore = [&](int buf, int p) {
+    const int valid = kv_len - p * kPage;  // keys of this page that exist (may exceed 64)
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      const int e = (tid + 256 * u) * 8;
+      *reinterpret_cast<bf16x8*>(&sK[buf][(e / DH) * KLD + (e % DH)]) = rk[u];
+      const int vr = e >> 6, vc = e & 63;  // V^T row (feature) and first key of the chunk
+      bf16x8 vv = rv[u];
+      if (vc + 8 > valid) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+          if (vc + t >= valid) vv[t] = (bf16)0.f;
+      }
+      *reinterpret_cast<bf16x8*>(&sV[buf][vr * VLD + vc]) = vv;
+    }
+  };
+
+  gload(0);
+  lstore(0, 0);
+  __syncthreads();
+  for (int p = 0; p < n_pages; ++p) {
+    const int buf = p & 1;
+    if (p + 1 < n_pages) gload(p + 1);
+    if (wave_active) {
+      floatx16 s[2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) s[kb][v] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < DH / 16; ++kk) {
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&sK[buf][(kb * 32 + l32) * KLD + 16 * kk + 8 * hi]);
+          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
+        }
+      }
+      // s[kb][v] holds key p*64 + kb*32 + 8*(v/4) + 4*hi + v%4 of query l32
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = p * kPage + kb * 32 + 8 * (v >> 2) + 4 * hi + (v & 3);
+          float x = s[kb][v] * scale_log2;
+          bool ok = key < kv_len;
+          if (CAUSAL) {
+            ok = ok && key <= qpos;
+            if (R > 0) x += rel[h * R + min(max(qpos - key, 0), R - 1)] * kLog2e;
+          }
+          x = ok ? x : -INFINITY;
+          s[kb][v] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run, mx);
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      const float alpha = exp2f(m_run - m_use);
+      float rs = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float e = exp2f(s[kb][v] - m_use);
+          s[kb][v] = e;
+          rs += e;
+        }
+      rs += __shfl_xor(rs, 32);
+      l_run = l_run * alpha + rs;
+      m_run = m_new;
+#pragma unroll
+      for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+      // O^T[d][q] += V^T[d][key] P^T[key][q]; k-step ks covers keys kb*32 + 16*half .. +16,
+      // MFMA k index 8*hi + t <-> key base + 8*(t/4) + 4*hi + t%4 on both operands
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int kb = ks >> 1, half = ks & 1;
+        bf16x8 pf;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) pf[t] = (bf16)s[kb][8 * half + t];
+        const int kbase = kb * 32 + 16 * half + 4 * hi;
+#pragma unroll
+        for (int db = 0; db < DH / 32; ++db) {
+          const bf16* vr = &sV[buf][(32 * db + l32) * VLD + kbase];
+          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vr);
+          const bf16x4 up = *reinterpret_cast<const bf16x4*>(vr + 8);
+          const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[db], 0, 0, 0);
+        }
+      }
+    }
+    if (p + 1 < n_pages) lstore(buf ^ 1, p + 1);
+    __syncthreads();
+  }
+
+  if (q_valid) {
+    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+    bf16* orow = out + (size_t)row * ldo + h * DH;
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        bf16x4 w;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w[t] = (bf16)(o[db][4 * gq + t] * inv);
+        *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * gq + 4 * hi) = w;
+      }
+  }
+}
+
+// ============================================================================
+// Plain paged attention (fp32 models, head widths without an MFMA variant).
+// 64 queries per block, 4 lanes per query, each lane owning dh/4 features;
+// pages staged in LDS; keys processed one at a time with the online softmax.
+// ============================================================================
+template <typename T, int DH>
+__global__ __launch_bounds__(256) void paged_attn_plain(const T* __restrict__ q, int ldq, T* __restrict__ out, int ldo,
+                                                        const T* __restrict__ pool, const int32_t* __restrict__ page_table,
+                                                        int max_pages, PageGeom g, int layer_slot,
+                                                        const AttnReq* __restrict__ reqs,
+                                                        const AttnTile* __restrict__ tiles, bool causal,
+                                                        const float* __restrict__ rel, int R, float scale_log2) {
+  constexpr int DP = DH / 4;
+  __shared__ float sK[kPage][DH + 1];
+  __shared__ float sV[DH][kPage + 1];
+  const AttnTile tile = tiles[blockIdx.x];
+  if (tile.q_count <= 0) return;
+  const AttnReq rq = reqs[tile.req];
+  const int h = tile.head, tid = threadIdx.x, qi = tid >> 2, part = tid & 3;
+  const bool active = qi < tile.q_count;
+  const int i = tile.q_begin + min(qi, tile.q_count - 1);
+  const int row = i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
+  const int qpos = rq.pos0 + i;
+
+  float qv[DP], acc[DP];
+#pragma unroll
+  for (int e = 0; e < DP; ++e) {
+    qv[e] = (float)q[(size_t)row * ldq + h * DH + part * DP + e];
+    acc[e] = 0.f;
+  }
+  float m_run = -INFINITY, l_run = 0.f;
+  const int kv_len = rq.kv_len;
+  int n_pages = (kv_len + kPage - 1) / kPage;
+  if (causal) n_pages = min(n_pages, (rq.pos0 + tile.q_begin + tile.q_count - 1) / kPage + 1);
+  const int32_t* ptab = page_table + (size_t)rq.slot * max_pages;
+
+  for (int p = 0; p < n_pages; ++p) {
+    const size_t base = (size_t)ptab[p] * g.page_elems;
+    const T* kp = pool + base + g.k_off(layer_slot, h);
+    const T* vp = pool + base + g.v_off(layer_slot, h);
+    const int valid = min(kPage, kv_len - p * kPage);
+    for (int e = tid; e < kPage * DH; e += 256) {
+      sK[e / DH][e % DH] = (float)kp[e];
+      const int vr = e / kPage, vc = e % kPage;
+      sV[vr][vc] = vc < valid ? (float)vp[e] : 0.f;
+    }
+    __syncthreads();
+    if (active) {
+      for (int j = 0; j < valid; ++j) {
+        const int key = p * kPage + j;
+        if (causal && key > qpos) break;
+        float s = 0.f;
+#pragma unroll
+        for (int e = 0; e < DP; ++e) s = fmaf(qv[e], sK[j][part * DP + e], s);
+        s += __shfl_xor(s, 1);
+        s += __shfl_xor(s, 2);
+        s *= scale_log2;
+        if (causal && R > 0) s += rel[h * R + min(qpos - key, R - 1)] * kLog2e;
+        const float m_new = fmaxf(m_run, s);
+        const float alpha = exp2f(m_run - m_new);
+        const float pj = exp2f(s - m_new);
+        l_run = l_run * alpha + pj;
+#pragma unroll
+        for (int e = 0; e < DP; ++e) acc[e] = fmaf(pj, sV[part * DP + e][j], acc[e] * alpha);
+        m_run = m_new;
+      }
+    }
+    __syncthreads();
+  }
+  if (active) {
+    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+#pragma unroll
+    for (int e = 0; e < DP; ++e) out[(size_t)row * ldo + h * DH + part * DP + e] = (T)(acc[e] * inv);
+  }
+}
+
+int paged_attention_q_block(bool bf, int dh) { return (bf && (dh == 64 || dh == 128)) ? 128 : 64; }
+
+hipError_t launch_paged_attention(bool bf, const void* q, int ldq, void* out, int ldo, const void* pool,
+                                  const int32_t* page_table, int max_pages, PageGeom g, int layer_slot,
+                                  const AttnReq* reqs, const AttnTile* tiles, int n_tiles, bool causal,
+                                  const float* rel, int R, int q_block, hipStream_t s) {
+  if (n_tiles <= 0) return hipSuccess;
+  const float sl2 = kLog2e / sqrtf((float)g.dh);
+  if (q_block != paged_attention_q_block(bf, g.dh)) return hipErrorInvalidValue;
+  if (bf && (g.dh == 64 || g.dh == 128)) {
+    const bf16* qq = (const bf16*)q;
+    bf16* oo = (bf16*)out;
+    const bf16* pp = (const bf16*)pool;
+#define TX_PA(DH, CZ)                                                                                              \
+  paged_attn_mfma<DH, CZ><<<n_tiles, 256, 0, s>>>(qq, ldq, oo, ldo, pp, page_table, max_pages, g, layer_slot, reqs, \
+                                                   tiles, rel, R, sl2)
+    if (g.dh == 64) {
+      if (causal) TX_PA(64, true); else TX_PA(64, false);
+    } else {
+      if (causal) TX_PA(128, true); else TX_PA(128, false);
+    }
+#undef TX_PA
+    return hipGetLastError();
+  }
+#define TX_PP(T, DH)                                                                                              \
+  paged_attn_plain<T, DH><<<n_tiles, 256, 0, s>>>((const T*)q, ldq, (T*)out, ldo, (const T*)pool, page_table,     \
+                                                  max_pages, g, layer_slot, reqs, tiles, causal, rel, R, sl2)
+  if (bf) {
+    if (g.dh == 32) TX_PP(bf16, 32); else if (g.dh == 64) TX_PP(bf16, 64); else if (g.dh == 128) TX_PP(bf16, 128);
+    else return hipErrorInvalidValue;
+  } else {
+    if (g.dh == 32) TX_PP(float, 32); else if (g.dh == 64) TX_PP(float, 64); else if (g.dh == 128) TX_PP(float, 128);
+    else return hipErrorInvalidValue;
+  }
+#undef TX_PP
+  return hipGetLastError();
+}
+
+// ============================================================================
+// Decoder self-attention (App. B mask). 64 queries per block, 4 lanes per
+// query. Serving keys/values are staged 64 at a time in LDS; a candidate then
+// adds its own key/value, read from its row.
+// ============================================================================
+template <typename T, int DH>
+__global__ __launch_bounds__(256) void self_attn_plain(const T* __restrict__ qkv, int d, T* __restrict__ out,
+                                                       const SelfReq* __restrict__ reqs,
+                                                       const SelfTile* __restrict__ tiles, bool cand_only,
+                                                       float scale_log2) {
+  constexpr int DP = DH / 4;
+  __shared__ float sK[64][DH + 1];
+  __shared__ float sV[64][DH + 1];
+  const SelfTile tile = tiles[blockIdx.x];
+  if (tile.q_count <= 0) return;
+  const SelfReq rq = reqs[tile.req];
+  const int h = tile.head, tid = threadIdx.x, qi = tid >> 2, part = tid & 3;
+  const int ld = 3 * d;
+  const bool active = qi < tile.q_count;
+  const int i = tile.q_begin + min(qi, tile.q_count - 1);
+  bool is_cand;
+  int row;
+  if (cand_only) {
+    is_cand = true;
+    row = rq.c_row + i;
+  } else {
+    is_cand = i >= rq.S;
+    row = is_cand ? rq.c_row + (i - rq.S) : rq.s_row + i;
+  }
+  const int visible = is_cand ? rq.S : i + 1;  // serving keys this query sees
+
+  float qv[DP], acc[DP];
+#pragma unroll
+  for (int e = 0; e < DP; ++e) {
+    qv[e] = (float)qkv[(size_t)row * ld + h * DH + part * DP + e];
+    acc[e] = 0.f;
+  }
+  float m_run = -INFINITY, l_run = 0.f;
+  auto consume = [&](float s, const float* vrow_part, int vstride) {
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    s *= scale_log2;
+    const float m_new = fmaxf(m_run, s);
+    const float alpha = exp2f(m_run - m_new);
+    const float pj = exp2f(s - m_new);
+    l_run = l_run * alpha + pj;
+#pragma unroll
+    for (int e = 0; e < DP; ++e) acc[e] = fmaf(pj, vrow_part[e * vstride], acc[e] * alpha);
+    m_run = m_new;
+  };
+
+  for (int c0 = 0; c0 < rq.S; c0 += 64) {
+    const int nk = min(64, rq.S - c0);
+    for (int e = tid; e < nk * DH; e += 256) {
+      const int j = e / DH, f = e % DH;
+      const size_t r = (size_t)(rq.s_row + c0 + j) * ld;
+      sK[j][f] = (float)qkv[r + d + h * DH + f];
+      sV[j][f] = (float)qkv[r + 2 * d + h * DH + f];
+    }
+    __syncthreads();
+    if (active) {
+      const int jmax = min(nk, visible - c0);
+      for (int j = 0; j < jmax; ++j) {
+        float s = 0.f;
+#pragma unroll
+        for (int e = 0; e < DP; ++e) s = fmaf(qv[e], sK[j][part * DP + e], s);
+        consume(s, &sV[j][part * DP], 1);
+      }
+    }
+    __syncthreads();
+  }
+  if (active && is_cand) {
+    float kv[DP], vv[DP];
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < DP; ++e) {
+      kv[e] = (float)qkv[(size_t)row * ld + d + h * DH + part * DP + e];
+      vv[e] = (float)qkv[(size_t)row * ld + 2 * d + h * DH + part * DP + e];
+      s = fmaf(qv[e], kv[e], s);
+    }
+    consume(s, vv, 1);
+  }
+  if (active) {
+    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+#pragma unroll
+    for (int e = 0; e < DP; ++e) out[(size_t)row * d + h * DH + part * DP + e] = (T)(acc[e] * inv);
+  }
+}
+
+int self_attention_q_block() { return 64; }
+
+hipError_t launch_self_attention(bool bf, const void* qkv, int d, int H, void* out, const SelfReq* reqs,
+                                 const SelfTile* tiles, int n_tiles, bool candidates_only, hipStream_t s) {
+  if (n_tiles <= 0) return hipSuccess;
+  const int dh = d / H;
+  const float sl2 = kLog2e / sqrtf((float)dh);
+#define TX_SA(T, DH)                                                                                             \
+  self_attn_plain<T, DH><<<n_tiles, 256, 0, s>>>((const T*)qkv, d, (T*)out, reqs, tiles, candidates_only, sl2)
+  if (bf) {
+    if (dh == 32) TX_SA(bf16, 32); else if (dh == 64) TX_SA(bf16, 64); else if (dh == 128) TX_SA(bf16, 128);
+    else return hipErrorInvalidValue;
+  } else {
+    if (dh == 32) TX_SA(float, 32); else if (dh == 64) TX_SA(float, 64); else if (dh == 128) TX_SA(float, 128);
+    else return hipErrorInvalidValue;
+  }
+#undef TX_SA
+  return hipGetLastError();
+}
+
+}  // namespace tx

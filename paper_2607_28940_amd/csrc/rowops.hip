@@ -1,0 +1,240 @@
+// Row-wise and data-movement kernels of the TransX path:
+//   LayerNorm of post-LN sublayers (Sec. 4.1.2 crossAttend block), optionally
+//   fused with the linear scoring head (Sec. 4.1.3, Eq. action-decoding with
+//   two actions reduces to one logit), the scatter of projected K/V rows into
+//   the paged cache layout, cache export, and weight repacking.
+#include "tx_internal.h"
+
+namespace tx {
+
+// One wave per row; EPL features per lane held in registers (EPL = d / 64).
+// Two-pass mean / variance in fp32 from the register copy.
+template <typename T, int EPL, bool SCORE>
+__global__ __launch_bounds__(256) void layernorm_rows(const T* __restrict__ x, T* __restrict__ y,
+                                                      const float* __restrict__ g, const float* __restrict__ b,
+                                                      const float* __restrict__ w, const float* __restrict__ b0,
+                                                      float* __restrict__ scores, int M, int d, float eps) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= M) return;
+  const T* xr = x + (size_t)row * d + lane * EPL;
+  float v[EPL];
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) v[e] = (float)xr[e];
+  float sum = 0.f;
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) sum += v[e];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+  const float mean = sum / d;
+  float sq = 0.f;
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) {
+    const float t = v[e] - mean;
+    sq += t * t;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) sq += __shfl_xor(sq, o);
+  const float inv = rsqrtf(sq / d + eps);
+  const int c0 = lane * EPL;
+  if (SCORE) {
+    float dot = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) dot += ((v[e] - mean) * inv * g[c0 + e] + b[c0 + e]) * w[c0 + e];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) dot += __shfl_xor(dot, o);
+    if (lane == 0) scores[row] = dot + b0[0];
+  } else {
+    T* yr = y + (size_t)row * d + c0;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) yr[e] = (T)((v[e] - mean) * inv * g[c0 + e] + b[c0 + e]);
+  }
+}
+
+// Generic width: one wave per row, strided features, three passes over the row.
+template <typename T, bool SCORE>
+__global__ __launch_bounds__(256) void layernorm_rows_any(const T* __restrict__ x, T* __restrict__ y,
+                                                          const float* __restrict__ g, const float* __restrict__ b,
+                                                          const float* __restrict__ w, const float* __restrict__ b0,
+                                                          float* __restrict__ scores, int M, int d, float eps) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= M) return;
+  const T* xr = x + (size_t)row * d;
+  float sum = 0.f;
+  for (int c = lane; c < d; c += 64) sum += (float)xr[c];
+  for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+  const float mean = sum / d;
+  float sq = 0.f;
+  for (int c = lane; c < d; c += 64) {
+    const float t = (float)xr[c] - mean;
+    sq += t * t;
+  }
+  for (int o = 32; o >= 1; o >>= 1) sq += __shfl_xor(sq, o);
+  const float inv = rsqrtf(sq / d + eps);
+  float dot = 0.f;
+  for (int c = lane; c < d; c += 64) {
+    const float z = ((float)xr[c] - mean) * inv * g[c] + b[c];
+    if (SCORE) dot += z * w[c];
+    else y[(size_t)row * d + c] = (T)z;
+  }
+  if (SCORE) {
+    for (int o = 32; o >= 1; o >>= 1) dot += __shfl_xor(dot, o);
+    if (lane == 0) scores[row] = dot + b0[0];
+  }
+}
+
+template <typename T, bool SCORE>
+static hipError_t ln_dispatch(const void* x, void* y, const float* g, const float* b, const float* w, const float* b0,
+                              float* scores, int M, int d, float eps, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  const int blocks = (M + 3) / 4;
+  const T* xx = (const T*)x;
+  T* yy = (T*)y;
+#define TX_LN(E) layernorm_rows<T, E, SCORE><<<blocks, 256, 0, s>>>(xx, yy, g, b, w, b0, scores, M, d, eps)
+  switch (d) {
+    case 64: TX_LN(1); break;
+    case 128: TX_LN(2); break;
+    case 256: TX_LN(4); break;
+    case 512: TX_LN(8); break;
+    case 1024: TX_LN(16); break;
+    case 2048: TX_LN(32); break;
+    default: layernorm_rows_any<T, SCORE><<<blocks, 256, 0, s>>>(xx, yy, g, b, w, b0, scores, M, d, eps);
+  }
+#undef TX_LN
+  return hipGetLastError();
+}
+
+hipError_t launch_layernorm(bool bf, const void* x, void* y, const float* g, const float* b, int M, int d, float eps,
+                            hipStream_t s) {
+  return bf ? ln_dispatch<bf16, false>(x, y, g, b, nullptr, nullptr, nullptr, M, d, eps, s)
+            : ln_dispatch<float, false>(x, y, g, b, nullptr, nullptr, nullptr, M, d, eps, s);
+}
+
+hipError_t launch_layernorm_score(bool bf, const void* x, const float* g, const float* b, const float* w,
+                                  const float* b0, float* scores, int M, int d, float eps, hipStream_t s) {
+  return bf ? ln_dispatch<bf16, true>(x, nullptr, g, b, w, b0, scores, M, d, eps, s)
+            : ln_dispatch<float, true>(x, nullptr, g, b, w, b0, scores, M, d, eps, s);
+}
+
+// ---------------------------------------------------------------- cache scatter
+// One thread per (row, layer, K|V, head, 8-feature chunk). The row's request is
+// found by binary search over the requests' first rows (ascending).
+template <typename T>
+__global__ __launch_bounds__(256) void scatter_kv(const T* __restrict__ src, int lds, int n_layers, int slot0,
+                                                  T* __restrict__ pool, const int32_t* __restrict__ page_table,
+                                                  int max_pages, PageGeom g, const ScatterReq* __restrict__ reqs,
+                                                  int n_req, int64_t n_items) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= n_items) return;
+  const int chunks = g.dh / 8;
+  const int per_row = n_layers * 2 * g.H * chunks;
+  const int row = (int)(idx / per_row);
+  int rem = (int)(idx % per_row);
+  const int ch = rem % chunks;
+  rem /= chunks;
+  const int h = rem % g.H;
+  rem /= g.H;
+  const int kind = rem & 1;
+  const int layer = rem >> 1;
+  int lo = 0, hi = n_req - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (reqs[mid].row0 <= row) lo = mid;
+    else hi = mid - 1;
+  }
+  const ScatterReq rq = reqs[lo];
+  const int pos = rq.pos0 + (row - rq.row0);
+  const int d = g.H * g.dh;
+  const T* s = src + (size_t)row * lds + (size_t)layer * 2 * d + kind * d + h * g.dh + ch * 8;
+  T* base = pool + (size_t)page_table[(size_t)rq.slot * max_pages + pos / kPage] * g.page_elems;
+  const int t = pos % kPage;
+  if (kind == 0) {
+    T* dst = base + g.k_off(slot0 + layer, h) + (size_t)t * g.dh + ch * 8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dst[e] = s[e];
+  } else {
+    T* dst = base + g.v_off(slot0 + layer, h) + (size_t)(ch * 8) * kPage + t;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dst[(size_t)e * kPage] = s[e];
+  }
+}
+
+hipError_t launch_scatter_kv(bool bf, const void* src, int lds, int n_layers, int slot0, void* pool,
+                             const int32_t* page_table, int max_pages, PageGeom g, const ScatterReq* reqs, int n_req,
+                             int n_rows, hipStream_t s) {
+  if (n_rows <= 0 || n_req <= 0) return hipSuccess;
+  const int64_t n_items = (int64_t)n_rows * n_layers * 2 * g.H * (g.dh / 8);
+  const int64_t blocks = (n_items + 255) / 256;
+  if (bf)
+    scatter_kv<bf16><<<(unsigned)blocks, 256, 0, s>>>((const bf16*)src, lds, n_layers, slot0, (bf16*)pool, page_table,
+                                                      max_pages, g, reqs, n_req, n_items);
+  else
+    scatter_kv<float><<<(unsigned)blocks, 256, 0, s>>>((const float*)src, lds, n_layers, slot0, (float*)pool,
+                                                       page_table, max_pages, g, reqs, n_req, n_items);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- cache export
+template <typename T>
+__global__ __launch_bounds__(256) void export_kv(const T* __restrict__ pool, const int32_t* __restrict__ page_row,
+                                                 PageGeom g, int layer_slot, int is_v, int64_t len,
+                                                 T* __restrict__ out) {
+  const int d = g.H * g.dh;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= len * d) return;
+  const int64_t pos = idx / d;
+  const int c = (int)(idx % d), h = c / g.dh, f = c % g.dh;
+  const T* base = pool + (size_t)page_row[pos / kPage] * g.page_elems;
+  const int t = (int)(pos % kPage);
+  out[idx] = is_v ? base[g.v_off(layer_slot, h) + (size_t)f * kPage + t] : base[g.k_off(layer_slot, h) + (size_t)t * g.dh + f];
+}
+
+hipError_t launch_export_kv(bool bf, const void* pool, const int32_t* page_row, PageGeom g, int layer_slot, int is_v,
+                            int64_t len, void* out, hipStream_t s) {
+  const int64_t n = len * g.H * g.dh;
+  if (n <= 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((n + 255) / 256);
+  if (bf) export_kv<bf16><<<blocks, 256, 0, s>>>((const bf16*)pool, page_row, g, layer_slot, is_v, len, (bf16*)out);
+  else export_kv<float><<<blocks, 256, 0, s>>>((const float*)pool, page_row, g, layer_slot, is_v, len, (float*)out);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- weight repack
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_tiles(const T* __restrict__ src, T* __restrict__ dst, int K, int N,
+                                                       int dst_ld) {
+  __shared__ T tile[32][33];
+  const int n0 = blockIdx.x * 32, k0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
+  for (int r = ty; r < 32; r += 8) {
+    const int k = k0 + r, n = n0 + tx;
+    if (k < K && n < N) tile[r][tx] = src[(size_t)k * N + n];
+  }
+  __syncthreads();
+  for (int r = ty; r < 32; r += 8) {
+    const int n = n0 + r, k = k0 + tx;
+    if (k < K && n < N) dst[(size_t)n * dst_ld + k] = tile[tx][r];
+  }
+}
+
+hipError_t launch_transpose(bool bf, const void* src, void* dst, int K, int N, int dst_ld, hipStream_t s) {
+  dim3 grid((N + 31) / 32, (K + 31) / 32);
+  if (bf) transpose_tiles<bf16><<<grid, 256, 0, s>>>((const bf16*)src, (bf16*)dst, K, N, dst_ld);
+  else transpose_tiles<float><<<grid, 256, 0, s>>>((const float*)src, (float*)dst, K, N, dst_ld);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void to_f32_kernel(const T* __restrict__ src, float* __restrict__ dst, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) dst[i] = (float)src[i];
+}
+
+hipError_t launch_to_f32(bool bf, const void* src, float* dst, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((n + 255) / 256);
+  if (bf) to_f32_kernel<bf16><<<blocks, 256, 0, s>>>((const bf16*)src, dst, n);
+  else to_f32_kernel<float><<<blocks, 256, 0, s>>>((const float*)src, dst, n);
+  return hipGetLastError();
+}
+
+}  // namespace tx

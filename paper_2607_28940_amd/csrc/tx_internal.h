@@ -1,0 +1,112 @@
+// Internal declarations of the TransX HIP library: element types, device
+// helpers, the metadata records the host hands to kernels, and the launch
+// functions each kernel file exports to the API layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tx {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kPage = 64;  // tokens per cache page
+
+// ------------------------------------------------------------ metadata records
+
+// One request as seen by an attention launch. Query i of the request lives in
+// activation row (i < qa_n ? qa_row + i : qb_row + i - qa_n); when causal it sits
+// at sequence position pos0 + i. Keys are cache positions 0 .. kv_len-1 of the
+// request whose page-table row is `slot`.
+struct AttnReq {
+  int32_t qa_row, qa_n, qb_row, qb_n;
+  int32_t kv_len, pos0, slot, pad;
+};
+
+// A unit of attention work: queries q_begin .. q_begin+q_count-1 of request
+// `req` (index into the AttnReq array) for head `head`.
+struct AttnTile {
+  int32_t req, head, q_begin, q_count;
+};
+
+// One request of the decoder self-attention: serving rows s_row .. s_row+S-1
+// (causal among themselves), candidate rows c_row .. c_row+C-1 (see every
+// serving row and themselves).
+struct SelfReq {
+  int32_t s_row, S, c_row, C;
+};
+
+// Self-attention tile: queries q_begin.. (in the request's [serving; candidate]
+// order) of request `req`, head `head`.
+typedef AttnTile SelfTile;
+
+// Rows to scatter into cache pages: rows row0 .. row0+n-1 of the source matrix
+// take sequence positions pos0 .. pos0+n-1 of the request in page-table row slot.
+struct ScatterReq {
+  int32_t row0, n, pos0, slot;
+};
+
+// Geometry of a cache page: for each layer slot (encoder layers, then decoder
+// layers), K as [H][64][dh] then V transposed as [H][dh][64].
+struct PageGeom {
+  int32_t H, dh, n_slots;
+  int64_t page_elems;  // elements per page
+  __host__ __device__ int64_t k_off(int slot, int h) const {
+    return ((int64_t)(slot * 2 + 0) * H + h) * kPage * dh;
+  }
+  __host__ __device__ int64_t v_off(int slot, int h) const {
+    return ((int64_t)(slot * 2 + 1) * H + h) * kPage * dh;
+  }
+};
+
+// ------------------------------------------------------------ launch functions
+// Every launcher returns hipSuccess or the launch error. Element type of the
+// activations is given by `bf16` (true) or fp32 (false).
+
+enum Epilogue { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2 };
+
+// C[M][N] (ldc) = epi(A[M][K] (lda) * Bt[N][K]^T + bias[N] (+ R[M][N] (ldr)))
+hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const float* bias, const void* R, int ldr,
+                       void* C, int ldc, int M, int N, int K, Epilogue epi, hipStream_t s);
+
+// y[i] = LN(x[i]) * g + b over d features, rows row0 .. row0+M-1
+hipError_t launch_layernorm(bool bf, const void* x, void* y, const float* g, const float* b, int M, int d,
+                            float eps, hipStream_t s);
+// scores[i] = LN(x[i]) . w + b0 (fp32)
+hipError_t launch_layernorm_score(bool bf, const void* x, const float* g, const float* b, const float* w,
+                                  const float* b0, float* scores, int M, int d, float eps, hipStream_t s);
+
+// Paged attention: out[row] = softmax(q k^T / sqrt(dh) (+ rel bias)) v over the
+// request's cached keys (causal: keys at positions <= the query's position).
+hipError_t launch_paged_attention(bool bf, const void* q, int ldq, void* out, int ldo, const void* pool,
+                                  const int32_t* page_table, int max_pages, PageGeom g, int layer_slot,
+                                  const AttnReq* reqs, const AttnTile* tiles, int n_tiles, bool causal,
+                                  const float* rel, int R, int q_block, hipStream_t s);
+// Query block (queries per tile) each attention kernel variant expects.
+int paged_attention_q_block(bool bf, int dh);
+
+// Decoder self-attention over the packed QKV matrix (ld 3d).
+hipError_t launch_self_attention(bool bf, const void* qkv, int d, int H, void* out, const SelfReq* reqs,
+                                 const SelfTile* tiles, int n_tiles, bool candidates_only, hipStream_t s);
+int self_attention_q_block();
+
+// Write K and V columns of src (per layer: K in cols [l*2d, l*2d+d), V in
+// [l*2d+d, l*2d+2d); ld = lds) into the pages of layer slots slot0 .. slot0+n_layers-1.
+hipError_t launch_scatter_kv(bool bf, const void* src, int lds, int n_layers, int slot0, void* pool,
+                             const int32_t* page_table, int max_pages, PageGeom g, const ScatterReq* reqs,
+                             int n_req, int n_rows, hipStream_t s);
+// Export one cached tensor (K or V of a layer slot) of a request into a dense
+// [len][H*dh] matrix.
+hipError_t launch_export_kv(bool bf, const void* pool, const int32_t* page_row, PageGeom g, int layer_slot, int is_v,
+                            int64_t len, void* out, hipStream_t s);
+
+// dst[n][k] = src[k][n] (src [K][N] row-major), same element type
+hipError_t launch_transpose(bool bf, const void* src, void* dst, int K, int N, int dst_ld, hipStream_t s);
+// dst fp32[n] = src[n]
+hipError_t launch_to_f32(bool bf, const void* src, float* dst, int64_t n, hipStream_t s);
+
+}  // namespace tx
