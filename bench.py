@@ -97,6 +97,8 @@ def main():
     ap.add_argument("--no-profile", action="store_true", help="time without per-launch events")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="HBM bytes per launch from rocprofv3 counters (optional)")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="run one plain 1 GiB device copy first (reference for counter scaling)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -133,6 +135,12 @@ def main():
     torch.cuda.synchronize()
     print(f"# setup {time.time() - t_setup:.1f} s: {wl.B} caches built", file=sys.stderr, flush=True)
 
+    if args.calib_copy:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(args.warmup):
         cache.score(ids, xs, so, xc, co, out=out)
     torch.cuda.synchronize()

@@ -950,7 +950,7 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, int a, int b, const
     cand[i] = AttnReq{c_row, C, 0, 0, kv, 0, ids[r], 0};
     mx = std::max<int64_t>(mx, S + C);
   }
-  const int qb = paged_attention_q_block(bf, m->dh), sqb = self_attention_q_block();
+  const int qb = paged_attention_q_block(bf, m->dh), sqb = self_attention_q_block(bf, m->dh);
   std::vector<AttnTile> t_full, t_cand;
   std::vector<SelfTile> s_full, s_cand;
   if (m->n_dec > 1) {

@@ -20,6 +20,120 @@ namespace tx {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+
+// Running state of one wave's 32 queries: O^T accumulators (rows = features,
+// columns = queries), running max and sum (base-2 domain).
+template <int DH>
+struct MfmaAcc {
+  floatx16 o[DH / 32];
+  float m, l;
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
+    m = -INFINITY;
+    l = 0.f;
+  }
+};
+
+// V^T tiles in LDS hold each 16-key group in the order 0-3, 8-11, 4-7, 12-15
+// (vt_pos maps a key to its column), so that the 8 keys one lane needs for a
+// PV fragment are contiguous.
+__device__ __forceinline__ int vt_pos(int key) {
+  return (key & ~15) | (key & 3) | ((key & 4) << 1) | ((key & 8) >> 1);
+}
+
+// One 64-key tile for one wave: S^T = K Q^T on MFMA (keys as rows, so lane
+// l32 + 32*hi holds 32 keys of query l32), online softmax update, then
+// O^T += V^T P^T with P^T taken from the S^T accumulators: the MFMA k index
+// 8*hi + t stands for key base + 8*(t/4) + 4*hi + t%4 on both operands, so no
+// register shuffle is needed, and the permuted V^T tile supplies exactly those
+// keys with one 16-byte LDS read.
+// The running max is kept in raw logit units, so scaling and max subtraction
+// fuse into one FMA before exp2. When `masked` (uniform across the wave) every
+// raw logit goes through `mask(key, s)`, which returns it (plus any bias, in
+// raw units) or -inf; other tiles skip that work. The O^T rescale is skipped when no lane's
+// max moved.
+template <int DH, int KLD, int VLD, class Mask>
+__device__ __forceinline__ void mfma_attend_tile(const bf16* __restrict__ sK, const bf16* __restrict__ sV,
+                                                 const bf16x8 (&qf)[DH / 16], MfmaAcc<DH>& acc, float scale_log2,
+                                                 int l32, int hi, bool masked, Mask mask) {
+  floatx16 s[2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s[kb][v] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < DH / 16; ++kk) {
+      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&sK[(kb * 32 + l32) * KLD + 16 * kk + 8 * hi]);
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
+    }
+  }
+  if (masked) {  // wave-uniform
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) s[kb][v] = mask(kb * 32 + 8 * (v >> 2) + 4 * hi + (v & 3), s[kb][v]);
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kb][v]);
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float m_new = fmaxf(acc.m, mx);
+  const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+  const float alpha = __builtin_amdgcn_exp2f((acc.m - m_use) * scale_log2);
+  const float off = -m_use * scale_log2;
+  float rs = 0.f;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const float e = __builtin_amdgcn_exp2f(fmaf(s[kb][v], scale_log2, off));
+      s[kb][v] = e;
+      rs += e;
+    }
+  rs += __shfl_xor(rs, 32);
+  acc.l = acc.l * alpha + rs;
+  acc.m = m_new;
+  if (__any(alpha != 1.f)) {
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc.o[db][v] *= alpha;
+  }
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const int kb = ks >> 1, half = ks & 1;
+    bf16x8 pf;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) pf[t] = (bf16)s[kb][8 * half + t];
+    const int kbase = kb * 32 + 16 * half + 8 * hi;  // in the V^T tile's permuted key order
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db) {
+      const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&sV[(32 * db + l32) * VLD + kbase]);
+      acc.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc.o[db], 0, 0, 0);
+    }
+  }
+}
+
+// Normalised output of a wave's queries: O[query l32][features] as bf16.
+template <int DH>
+__device__ __forceinline__ void mfma_store_out(const MfmaAcc<DH>& acc, bf16* __restrict__ orow, int hi) {
+  const float inv = acc.l > 0.f ? 1.f / acc.l : 0.f;
+#pragma unroll
+  for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      bf16x4 w;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) w[t] = (bf16)(acc.o[db][4 * gq + t] * inv);
+      *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * gq + 4 * hi) = w;
+    }
+}
+
 // ============================================================================
 // bf16 paged attention on MFMA.
 //
@@ -65,6 +179,7 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
   const int i = tile.q_begin + min(qi, tile.q_count - 1);
   const int row = i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
   const int qpos = rq.pos0 + i;
+  const float bias_scale = kLog2e / scale_log2;  // logit bias expressed in raw q.k units
 
   // Q as the MFMA B operand: lane holds Q[query l32][16*kk + 8*hi .. +8]
   bf16x8 qf[DH / 16];
@@ -74,12 +189,8 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
     for (int kk = 0; kk < DH / 16; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qr + 16 * kk);
   }
 
-  floatx16 o[DH / 32];
-#pragma unroll
-  for (int db = 0; db < DH / 32; ++db)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+  MfmaAcc<DH> acc;
+  acc.init();
 
   const int kv_len = rq.kv_len;
   int n_pages = (kv_len + kPage - 1) / kPage;
@@ -108,12 +219,15 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
       *reinterpret_cast<bf16x8*>(&sK[buf][(e / DH) * KLD + (e % DH)]) = rk[u];
       const int vr = e >> 6, vc = e & 63;  // V^T row (feature) and first key of the chunk
       bf16x8 vv = rv[u];
-      if (vc + 8 > valid) {
+      if (valid < kPage) {  // only the request's last page is partial (uniform branch)
 #pragma unroll
         for (int t = 0; t < 8; ++t)
           if (vc + t >= valid) vv[t] = (bf16)0.f;
       }
-      *reinterpret_cast<bf16x8*>(&sV[buf][vr * VLD + vc]) = vv;
+      // keys vc..vc+3 and vc+4..vc+7 land at their permuted columns
+      bf16* vrow = &sV[buf][vr * VLD];
+      *reinterpret_cast<bf16x4*>(vrow + vt_pos(vc)) = bf16x4{vv[0], vv[1], vv[2], vv[3]};
+      *reinterpret_cast<bf16x4*>(vrow + vt_pos(vc + 4)) = bf16x4{vv[4], vv[5], vv[6], vv[7]};
     }
   };
 
@@ -124,90 +238,125 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
     const int buf = p & 1;
     if (p + 1 < n_pages) gload(p + 1);
     if (wave_active) {
-      floatx16 s[2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) s[kb][v] = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < DH / 16; ++kk) {
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&sK[buf][(kb * 32 + l32) * KLD + 16 * kk + 8 * hi]);
-          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
+      const int key0 = p * kPage;
+      // masking is needed on the request's last (partial) page and, when
+      // causal, on pages that reach past this wave's first query position;
+      // the relative-position bias applies to every causal tile
+      const bool needs_mask = CAUSAL || key0 + kPage > kv_len;
+      auto mask = [&](int kl, float x) {
+        const int key = key0 + kl;
+        bool ok = key < kv_len;
+        if (CAUSAL) {
+          ok = ok && key <= qpos;
+          if (R > 0) x += rel[h * R + min(max(qpos - key, 0), R - 1)] * bias_scale;
         }
-      }
-      // s[kb][v] holds key p*64 + kb*32 + 8*(v/4) + 4*hi + v%4 of query l32
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = p * kPage + kb * 32 + 8 * (v >> 2) + 4 * hi + (v & 3);
-          float x = s[kb][v] * scale_log2;
-          bool ok = key < kv_len;
-          if (CAUSAL) {
-            ok = ok && key <= qpos;
-            if (R > 0) x += rel[h * R + min(max(qpos - key, 0), R - 1)] * kLog2e;
-          }
-          x = ok ? x : -INFINITY;
-          s[kb][v] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = exp2f(m_run - m_use);
-      float rs = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float e = exp2f(s[kb][v] - m_use);
-          s[kb][v] = e;
-          rs += e;
-        }
-      rs += __shfl_xor(rs, 32);
-      l_run = l_run * alpha + rs;
-      m_run = m_new;
-#pragma unroll
-      for (int db = 0; db < DH / 32; ++db)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
-      // O^T[d][q] += V^T[d][key] P^T[key][q]; k-step ks covers keys kb*32 + 16*half .. +16,
-      // MFMA k index 8*hi + t <-> key base + 8*(t/4) + 4*hi + t%4 on both operands
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const int kb = ks >> 1, half = ks & 1;
-        bf16x8 pf;
-#pragma unroll
-        for (int t = 0; t < 8; ++t) pf[t] = (bf16)s[kb][8 * half + t];
-        const int kbase = kb * 32 + 16 * half + 4 * hi;
-#pragma unroll
-        for (int db = 0; db < DH / 32; ++db) {
-          const bf16* vr = &sV[buf][(32 * db + l32) * VLD + kbase];
-          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vr);
-          const bf16x4 up = *reinterpret_cast<const bf16x4*>(vr + 8);
-          const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[db], 0, 0, 0);
-        }
-      }
+        return ok ? x : -INFINITY;
+      };
+      mfma_attend_tile<DH, KLD, VLD>(sK[buf], sV[buf], qf, acc, scale_log2, l32, hi, needs_mask, mask);
     }
     if (p + 1 < n_pages) lstore(buf ^ 1, p + 1);
     __syncthreads();
   }
+  if (q_valid) mfma_store_out<DH>(acc, out + (size_t)row * ldo + h * DH, hi);
+}
 
-  if (q_valid) {
-    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-    bf16* orow = out + (size_t)row * ldo + h * DH;
+// ============================================================================
+// bf16 decoder self-attention on MFMA (App. B mask). Same tile arithmetic as
+// the paged kernel: the request's serving tokens are the keys, staged 64 at a
+// time in LDS (K as rows, V transposed while it is written to LDS); serving
+// query i sees serving keys j <= i, every candidate sees all serving keys and
+// then its own key/value, folded in as one more online-softmax step.
+// ============================================================================
+template <int DH>
+__global__ __launch_bounds__(256, 2) void self_attn_mfma(const bf16* __restrict__ qkv, int d, bf16* __restrict__ out,
+                                                          const SelfReq* __restrict__ reqs,
+                                                          const SelfTile* __restrict__ tiles, bool cand_only,
+                                                          float scale_log2) {
+  constexpr int KLD = DH + 8, VLD = 64 + 8, NCH = 64 * DH / 8 / 256;
+  __shared__ __attribute__((aligned(16))) bf16 sK[64 * KLD];
+  __shared__ __attribute__((aligned(16))) bf16 sV[DH * VLD];
+  const SelfTile tile = tiles[blockIdx.x];
+  if (tile.q_count <= 0) return;
+  const SelfReq rq = reqs[tile.req];
+  const int h = tile.head, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, hi = lane >> 5;
+  const int ld = 3 * d;
+  const int qi = wave * 32 + l32;
+  const bool wave_active = wave * 32 < tile.q_count;
+  const bool q_valid = qi < tile.q_count;
+  const int i = tile.q_begin + min(qi, tile.q_count - 1);
+  bool is_cand;
+  int row;
+  if (cand_only) {
+    is_cand = true;
+    row = rq.c_row + i;
+  } else {
+    is_cand = i >= rq.S;
+    row = is_cand ? rq.c_row + (i - rq.S) : rq.s_row + i;
+  }
+  const int visible = is_cand ? rq.S : i + 1;
+
+  bf16x8 qf[DH / 16];
+  {
+    const bf16* qr = qkv + (size_t)row * ld + h * DH + 8 * hi;
+#pragma unroll
+    for (int kk = 0; kk < DH / 16; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qr + 16 * kk);
+  }
+  MfmaAcc<DH> acc;
+  acc.init();
+
+  for (int c0 = 0; c0 < rq.S; c0 += 64) {
+    const int valid = rq.S - c0;
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      const int e = (tid + 256 * u) * 8;
+      const int key = e / DH, col = e % DH;
+      const size_t r = (size_t)(rq.s_row + c0 + min(key, valid - 1)) * ld + h * DH + col;
+      const bf16x8 kv = *reinterpret_cast<const bf16x8*>(qkv + r + d);
+      bf16x8 vv = *reinterpret_cast<const bf16x8*>(qkv + r + 2 * d);
+      if (key >= valid) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) vv[t] = (bf16)0.f;
+      }
+      *reinterpret_cast<bf16x8*>(&sK[key * KLD + col]) = kv;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) sV[(col + t) * VLD + vt_pos(key)] = vv[t];
+    }
+    __syncthreads();
+    if (wave_active)
+      mfma_attend_tile<DH, KLD, VLD>(sK, sV, qf, acc, scale_log2, l32, hi, true,
+                                     [&](int kl, float x) { return (c0 + kl < visible) ? x : -INFINITY; });
+    __syncthreads();
+  }
+
+  if (is_cand) {
+    // the candidate's own key: dot over this lane's half of the features, then
+    // the other half from lane l ^ 32 (same query)
+    const bf16* kr = qkv + (size_t)row * ld + d + h * DH + 8 * hi;
+    float dot = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < DH / 16; ++kk) {
+      const bf16x8 kv = *reinterpret_cast<const bf16x8*>(kr + 16 * kk);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) dot = fmaf((float)qf[kk][t], (float)kv[t], dot);
+    }
+    dot += __shfl_xor(dot, 32);
+    const float m_new = fmaxf(acc.m, dot);
+    const float alpha = exp2f((acc.m - m_new) * scale_log2);
+    const float pself = exp2f((dot - m_new) * scale_log2);
+    acc.l = acc.l * alpha + pself;
+    acc.m = m_new;
+    const bf16* vr = qkv + (size_t)row * ld + 2 * d + h * DH + 4 * hi;
 #pragma unroll
     for (int db = 0; db < DH / 32; ++db)
 #pragma unroll
       for (int gq = 0; gq < 4; ++gq) {
-        bf16x4 w;
+        const bf16x4 v4 = *reinterpret_cast<const bf16x4*>(vr + 32 * db + 8 * gq);
 #pragma unroll
-        for (int t = 0; t < 4; ++t) w[t] = (bf16)(o[db][4 * gq + t] * inv);
-        *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * gq + 4 * hi) = w;
+        for (int t = 0; t < 4; ++t) acc.o[db][4 * gq + t] = fmaf(pself, (float)v4[t], acc.o[db][4 * gq + t] * alpha);
       }
   }
+  if (q_valid) mfma_store_out<DH>(acc, out + (size_t)row * d + h * DH, hi);
 }
 
 // ============================================================================
@@ -413,13 +562,20 @@ __global__ __launch_bounds__(256) void self_attn_plain(const T* __restrict__ qkv
   }
 }
 
-int self_attention_q_block() { return 64; }
+int self_attention_q_block(bool bf, int dh) { return (bf && (dh == 64 || dh == 128)) ? 128 : 64; }
 
 hipError_t launch_self_attention(bool bf, const void* qkv, int d, int H, void* out, const SelfReq* reqs,
                                  const SelfTile* tiles, int n_tiles, bool candidates_only, hipStream_t s) {
   if (n_tiles <= 0) return hipSuccess;
   const int dh = d / H;
   const float sl2 = kLog2e / sqrtf((float)dh);
+  if (bf && (dh == 64 || dh == 128)) {
+    if (dh == 64)
+      self_attn_mfma<64><<<n_tiles, 256, 0, s>>>((const bf16*)qkv, d, (bf16*)out, reqs, tiles, candidates_only, sl2);
+    else
+      self_attn_mfma<128><<<n_tiles, 256, 0, s>>>((const bf16*)qkv, d, (bf16*)out, reqs, tiles, candidates_only, sl2);
+    return hipGetLastError();
+  }
 #define TX_SA(T, DH)                                                                                             \
   self_attn_plain<T, DH><<<n_tiles, 256, 0, s>>>((const T*)qkv, d, (T*)out, reqs, tiles, candidates_only, sl2)
   if (bf) {

@@ -92,7 +92,7 @@ int paged_attention_q_block(bool bf, int dh);
 // Decoder self-attention over the packed QKV matrix (ld 3d).
 hipError_t launch_self_attention(bool bf, const void* qkv, int d, int H, void* out, const SelfReq* reqs,
                                  const SelfTile* tiles, int n_tiles, bool candidates_only, hipStream_t s);
-int self_attention_q_block();
+int self_attention_q_block(bool bf, int dh);
 
 // Write K and V columns of src (per layer: K in cols [l*2d, l*2d+d), V in
 // [l*2d+d, l*2d+2d); ld = lds) into the pages of layer slots slot0 .. slot0+n_layers-1.
