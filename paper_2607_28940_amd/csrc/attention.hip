@@ -82,10 +82,22 @@ __device__ __forceinline__ void mfma_attend_tile(const bf16* __restrict__ sK, co
 #pragma unroll
     for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kb][v]);
   mx = fmaxf(mx, __shfl_xor(mx, 32));
-  const float m_new = fmaxf(acc.m, mx);
-  const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-  const float alpha = __builtin_amdgcn_exp2f((acc.m - m_use) * scale_log2);
-  const float off = -m_use * scale_log2;
+  // Lazy reference max: probabilities are exp2((s - m) * scale) against a
+  // reference m that only moves when this tile would push one above 2^8
+  // (fine for fp32 sums and bf16 P); O and l are rescaled only then. The
+  // final O / l does not depend on which reference was used.
+  const bool bump = mx > acc.m + 8.f / scale_log2;
+  if (__any(bump)) {
+    const float m_new = bump ? mx : acc.m;
+    const float alpha = __builtin_amdgcn_exp2f((acc.m - m_new) * scale_log2);  // 0 when acc.m = -inf
+    acc.l *= alpha;
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc.o[db][v] *= alpha;
+    acc.m = m_new;
+  }
+  const float off = (acc.m == -INFINITY) ? 0.f : -acc.m * scale_log2;
   float rs = 0.f;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
@@ -96,14 +108,7 @@ __device__ __forceinline__ void mfma_attend_tile(const bf16* __restrict__ sK, co
       rs += e;
     }
   rs += __shfl_xor(rs, 32);
-  acc.l = acc.l * alpha + rs;
-  acc.m = m_new;
-  if (__any(alpha != 1.f)) {
-#pragma unroll
-    for (int db = 0; db < DH / 32; ++db)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc.o[db][v] *= alpha;
-  }
+  acc.l += rs;
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
     const int kb = ks >> 1, half = ks & 1;
@@ -272,7 +277,7 @@ __global__ __launch_bounds__(256, 2) void self_attn_mfma(const bf16* __restrict_
                                                           const SelfReq* __restrict__ reqs,
                                                           const SelfTile* __restrict__ tiles, bool cand_only,
                                                           float scale_log2) {
-  constexpr int KLD = DH + 8, VLD = 64 + 8, NCH = 64 * DH / 8 / 256;
+  constexpr int KLD = DH + 8, VLD = 64 + 8;
   __shared__ __attribute__((aligned(16))) bf16 sK[64 * KLD];
   __shared__ __attribute__((aligned(16))) bf16 sV[DH * VLD];
   const SelfTile tile = tiles[blockIdx.x];
@@ -307,20 +312,33 @@ __global__ __launch_bounds__(256, 2) void self_attn_mfma(const bf16* __restrict_
 
   for (int c0 = 0; c0 < rq.S; c0 += 64) {
     const int valid = rq.S - c0;
+    // each thread moves a pair of adjacent keys x 8 features: K rows go to LDS
+    // as they are; V is transposed with 4-byte writes (the two keys of a pair
+    // stay adjacent in the permuted V^T order), 32 lanes filling one 128-byte
+    // V^T row segment, so neither store has bank conflicts
 #pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const int e = (tid + 256 * u) * 8;
-      const int key = e / DH, col = e % DH;
-      const size_t r = (size_t)(rq.s_row + c0 + min(key, valid - 1)) * ld + h * DH + col;
-      const bf16x8 kv = *reinterpret_cast<const bf16x8*>(qkv + r + d);
-      bf16x8 vv = *reinterpret_cast<const bf16x8*>(qkv + r + 2 * d);
-      if (key >= valid) {
+    for (int u = 0; u < DH / 64; ++u) {
+      const int c = tid + 256 * u;
+      const int pair = c & 31, col = (c >> 5) * 8;
+      const int k0 = 2 * pair;
+      bf16x8 kv[2], vv[2];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) vv[t] = (bf16)0.f;
+      for (int w = 0; w < 2; ++w) {
+        const size_t r = (size_t)(rq.s_row + c0 + min(k0 + w, valid - 1)) * ld + h * DH + col;
+        kv[w] = *reinterpret_cast<const bf16x8*>(qkv + r + d);
+        vv[w] = *reinterpret_cast<const bf16x8*>(qkv + r + 2 * d);
+        if (k0 + w >= valid) {
+#pragma unroll
+          for (int t = 0; t < 8; ++t) vv[w][t] = (bf16)0.f;
+        }
+        *reinterpret_cast<bf16x8*>(&sK[(k0 + w) * KLD + col]) = kv[w];
       }
-      *reinterpret_cast<bf16x8*>(&sK[key * KLD + col]) = kv;
+      const int vp = vt_pos(k0);
 #pragma unroll
-      for (int t = 0; t < 8; ++t) sV[(col + t) * VLD + vt_pos(key)] = vv[t];
+      for (int t = 0; t < 8; ++t) {
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        *reinterpret_cast<bf16x2*>(&sV[(col + t) * VLD + vp]) = bf16x2{vv[0][t], vv[1][t]};
+      }
     }
     __syncthreads();
     if (wave_active)

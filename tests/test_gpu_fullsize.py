@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 from paper_2607_28940_amd import inputs as I
-from tests.parity_util import BF16_TOL, GpuRun, log, oracle_request, score_err
+from tests.parity_util import BF16_TOL, GpuRun, log, oracle_request, score_err, tensor_err
 
 pytestmark = pytest.mark.gpu
 
@@ -63,3 +63,63 @@ def test_headline_full(oracle_mod):
     for r in (0, 128, 255):
         assert np.array_equal(g2[r], g[r][::-1]), r
     torch.cuda.empty_cache()
+
+
+@pytest.fixture(autouse=True)
+def _free_memory():
+    yield
+    import gc
+    import torch
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def test_ragged_full(oracle_mod):
+    """B=512 requests, L lognormal (median 2048) in [128, 16384], S in [1, 64],
+    C in [32, 1024], d=1024: the load-balancing workload, scored in one call.
+    Oracle on two sampled requests; the longest request (L = 16384) is checked
+    by batch independence: its scores from the batched call equal, bitwise,
+    those of a call that scores it alone."""
+    wl = I.workload("ragged")
+    w = I.make_weights(wl.model)
+    log(f"ragged: building {wl.B} caches, {sum(wl.L)} tokens")
+    run = GpuRun(wl, w)
+    _build_all(run, 64)
+    order = np.argsort(wl.L)
+    sampled = [int(order[0]), int(order[wl.B // 2 - 40])]
+    g = _check_sampled(run, oracle_mod.Oracle(wl.model, w), sampled, "ragged")
+    longest = int(order[-1])
+    alone = run.score([longest])[0]
+    assert np.array_equal(alone, g[longest])
+
+
+def test_append_full(oracle_mod):
+    """B=1024 users with L=8192 cached tokens; 16 events appended to every user
+    in one call through the incremental encoder; then S=32, C=256 scoring.
+    The oracle recomputes user 0 end to end on the re-encoded 8208-token
+    sequence; for user 1023 the appended cache is compared with a GPU rebuild
+    of all 8208 tokens."""
+    wl = I.workload("append")
+    w = I.make_weights(wl.model)
+    log("append: building 1024 caches of 8192 tokens")
+    run = GpuRun(wl, w, max_tokens=8192 + 16)
+    _build_all(run, 64)
+    run.append(list(range(wl.B)), ws_limit=8 << 30)
+    assert run.cache.length(0) == 8208 and run.cache.length(wl.B - 1) == 8208
+    g = run.score(list(range(wl.B)), ws_limit=8 << 30)
+    assert np.all(np.isfinite(np.concatenate(g)))
+    orc = oracle_mod.Oracle(wl.model, w)
+    o = oracle_request(orc, wl, 0, append=True)[0]
+    err = score_err(g[0], o)
+    log(f"append: user 0 vs oracle on the re-encoded sequence: max err {err['max']:.3e} p99 {err['p99']:.3e}")
+    assert err["max"] <= BF16_TOL, err
+    # the last user's appended cache equals a rebuild of all its tokens
+    last = wl.B - 1
+    appended = [run.cache.export(last, p, l).float().cpu().numpy() for p in range(4) for l in range(2)]
+    X = np.concatenate([I.request_tokens(wl, last, I.STREAM_BEHAVIOR), I.request_tokens(wl, last, I.STREAM_EVENTS)])
+    run.cache.release([last])
+    run.cache.build([last], run.dev(X), I.offsets([len(X)]))
+    rebuilt = [run.cache.export(last, p, l).float().cpu().numpy() for p in range(4) for l in range(2)]
+    for a, b in zip(appended, rebuilt):
+        assert tensor_err(a, b) < 1e-2
+    assert score_err(run.score([last])[0], g[last])["max"] < 1e-2
