@@ -86,6 +86,32 @@ def cpu_baseline(wl, weights, n_req: int):
                       f"({n_scores} scores, {elapsed:.1f} s), cache contents seeded N(0,1)"}
 
 
+KERNEL_SOURCES = {"cross_attention": "attention.hip", "self_attention": "attention.hip", "gemm": "gemm.hip",
+                  "layernorm": "rowops.hip", "scatter": "rowops.hip", "causal_attention": "attention.hip"}
+
+
+def kernel_source_sha(kernel_class: str):
+    import hashlib
+    for key, fn in KERNEL_SOURCES.items():
+        if key in kernel_class:
+            path = os.path.join(ROOT, "paper_2607_28940_amd", "csrc", fn)
+            return hashlib.sha256(open(path, "rb").read()).hexdigest()
+    return None
+
+
+def measured_traffic(path: str, kernel_class: str):
+    """HBM bytes per launch of `kernel_class` from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, or None when there is none or the
+    kernel's source has changed since the counters were taken."""
+    try:
+        rec = json.load(open(path)).get(kernel_class)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_sha256") != kernel_source_sha(kernel_class):
+        return None
+    return rec.get("bytes_per_launch")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -181,12 +207,7 @@ def main():
         avg_s = p["ms"] / p["launches"] / 1e3
         fl_launch, by_launch = p["flops"] / p["launches"], p["bytes"] / p["launches"]
         mfma = fl_launch > 0 and fl_launch / max(by_launch, 1) > peak * 1e12 / (PEAK_HBM_GBS * 1e9)
-        traffic = None
-        if os.path.exists(args.traffic_json):
-            try:
-                traffic = json.load(open(args.traffic_json)).get(dom)
-            except (OSError, ValueError):
-                traffic = None
+        traffic = measured_traffic(args.traffic_json, dom)
         if mfma:
             ach = fl_launch / avg_s / 1e12
             roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",

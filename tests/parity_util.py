@@ -37,7 +37,7 @@ def tensor_err(g, o) -> float:
     return float(np.abs(g - o).max() / rms)
 
 
-class GpuRun:
+class DeviceCase:
     """A model and cache for one workload on cuda:0."""
 
     def __init__(self, wl: I.Workload, weights, max_tokens: Optional[int] = None, extra_pages: int = 0,

@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 from paper_2607_28940_amd import inputs as I
-from tests.parity_util import BF16_TOL, GpuRun, log, oracle_request, score_err, tensor_err
+from tests.parity_util import BF16_TOL, DeviceCase, log, oracle_request, score_err, tensor_err
 
 pytestmark = pytest.mark.gpu
 
@@ -18,7 +18,7 @@ def _cuda():
     torch.cuda.set_device(0)
 
 
-def _build_all(run: GpuRun, chunk: int):
+def _build_all(run: DeviceCase, chunk: int):
     wl = run.wl
     for a in range(0, wl.B, chunk):
         run.build(list(range(a, min(wl.B, a + chunk))), ws_limit=8 << 30)
@@ -41,7 +41,7 @@ def test_uniform_full(oracle_mod):
     wl = I.workload("uniform")
     w = I.make_weights(wl.model)
     log("uniform: building 64 caches")
-    run = GpuRun(wl, w)
+    run = DeviceCase(wl, w)
     _build_all(run, 64)
     _check_sampled(run, oracle_mod.Oracle(wl.model, w), [0, 37, 63], "uniform")
 
@@ -54,7 +54,7 @@ def test_headline_full(oracle_mod):
     wl = I.workload("headline")
     w = I.make_weights(wl.model)
     log("headline: building 256 caches")
-    run = GpuRun(wl, w)
+    run = DeviceCase(wl, w)
     _build_all(run, 128)
     g = _check_sampled(run, oracle_mod.Oracle(wl.model, w), [201], "headline")
     # reversing every request's candidates reverses its scores, bitwise
@@ -83,7 +83,7 @@ def test_ragged_full(oracle_mod):
     wl = I.workload("ragged")
     w = I.make_weights(wl.model)
     log(f"ragged: building {wl.B} caches, {sum(wl.L)} tokens")
-    run = GpuRun(wl, w)
+    run = DeviceCase(wl, w)
     _build_all(run, 64)
     order = np.argsort(wl.L)
     sampled = [int(order[0]), int(order[wl.B // 2 - 40])]
@@ -102,7 +102,7 @@ def test_append_full(oracle_mod):
     wl = I.workload("append")
     w = I.make_weights(wl.model)
     log("append: building 1024 caches of 8192 tokens")
-    run = GpuRun(wl, w, max_tokens=8192 + 16)
+    run = DeviceCase(wl, w, max_tokens=8192 + 16)
     _build_all(run, 64)
     run.append(list(range(wl.B)), ws_limit=8 << 30)
     assert run.cache.length(0) == 8208 and run.cache.length(wl.B - 1) == 8208

@@ -6,7 +6,7 @@ import pytest
 
 from paper_2607_28940_amd import inputs as I
 from paper_2607_28940_amd.inputs import ModelConfig
-from tests.parity_util import BF16_TOL, FP32_TOL, GpuRun, log, oracle_request, score_err, tensor_err
+from tests.parity_util import BF16_TOL, FP32_TOL, DeviceCase, log, oracle_request, score_err, tensor_err
 
 pytestmark = pytest.mark.gpu
 
@@ -23,7 +23,7 @@ def O(oracle_mod):
     return oracle_mod
 
 
-def _compare_all(run: GpuRun, orc, reqs, tol, label, append=False):
+def _compare_all(run: DeviceCase, orc, reqs, tol, label, append=False):
     g = run.score(reqs)
     o = [oracle_request(orc, run.wl, r, append=append)[0] for r in reqs]
     err = score_err(np.concatenate(g), np.concatenate(o))
@@ -38,7 +38,7 @@ def test_tiny_fp32(O, variant):
     wl = I.workload("tiny")
     w = I.make_weights(wl.model, variant)
     log(f"tiny fp32 {variant}")
-    run = GpuRun(wl, w)
+    run = DeviceCase(wl, w)
     run.build([0])
     _compare_all(run, O.Oracle(wl.model, w), [0], FP32_TOL, f"tiny fp32 {variant}")
 
@@ -59,7 +59,7 @@ def test_bf16_ragged_vs_oracle(O, name, model):
     wl = I.custom_workload(model, cfg_id=31, **RAGGED)
     w = I.make_weights(model, ("sharp", "affine"))
     log(f"bf16 ragged {name}")
-    run = GpuRun(wl, w)
+    run = DeviceCase(wl, w)
     run.build(range(wl.B))
     _compare_all(run, O.Oracle(model, w), range(wl.B), BF16_TOL, f"bf16 ragged {name}")
 
@@ -68,7 +68,7 @@ def test_cache_contents_vs_oracle(O):
     model = SMALL_BF16[0][1]
     wl = I.custom_workload(model, cfg_id=32, L=[150, 64], S=[4, 4], C=[4, 4])
     w = I.make_weights(model, ("sharp", "affine"))
-    run = GpuRun(wl, w)
+    run = DeviceCase(wl, w)
     run.build([0, 1])
     orc = O.Oracle(model, w)
     for r in (0, 1):
@@ -87,12 +87,12 @@ def test_append_equals_rebuild(O):
     model = SMALL_BF16[0][1]
     wl = I.custom_workload(model, cfg_id=33, L=[60, 130], S=[6, 2], C=[9, 17], n_append=13)
     w = I.make_weights(model, ("sharp", "affine"))
-    inc = GpuRun(wl, w)
+    inc = DeviceCase(wl, w)
     inc.build([0, 1])
     inc.append([0, 1], 0, 5)     # 60 -> 65 crosses a page boundary
     inc.append([0, 1], 5, 13)
     assert inc.cache.length(0) == 73 and inc.cache.length(1) == 143
-    full = GpuRun(wl, w)
+    full = DeviceCase(wl, w)
     X = [np.concatenate([I.request_tokens(wl, r, I.STREAM_BEHAVIOR), I.request_tokens(wl, r, I.STREAM_EVENTS)])
          for r in (0, 1)]
     full.cache.build([0, 1], full.dev(np.concatenate(X)), I.offsets([len(x) for x in X]))
@@ -121,7 +121,7 @@ def test_candidates_independent_on_gpu():
     model = SMALL_BF16[1][1]
     wl = I.custom_workload(model, cfg_id=34, L=[100], S=[7], C=[150])
     w = I.make_weights(model, ("sharp",))
-    run = GpuRun(wl, w)
+    run = DeviceCase(wl, w)
     run.build([0])
     Xc = I.request_tokens(wl, 0, I.STREAM_CANDIDATES)
     base = run.score([0], cand=[Xc])[0]
@@ -137,10 +137,10 @@ def test_poisoned_pool_and_chunked_workspace():
     model = SMALL_BF16[0][1]
     wl = I.custom_workload(model, cfg_id=35, **RAGGED)
     w = I.make_weights(model, ("sharp",))
-    clean = GpuRun(wl, w, fill_byte=0)
+    clean = DeviceCase(wl, w, fill_byte=0)
     clean.build(range(wl.B))
     ref = np.concatenate(clean.score(range(wl.B)))
-    dirty = GpuRun(wl, w, fill_byte=0xFF, extra_pages=3)
+    dirty = DeviceCase(wl, w, fill_byte=0xFF, extra_pages=3)
     small = dirty.cache.workspace_min_bytes(0, wl.B, I.offsets(wl.L))
     dirty.build(range(wl.B), ws_limit=small)
     got = np.concatenate(dirty.score(range(wl.B)))
@@ -157,7 +157,7 @@ def test_status_codes_on_gpu():
     model = SMALL_BF16[1][1]
     wl = I.custom_workload(model, cfg_id=36, L=[64, 65], S=[1, 1], C=[2, 2])
     w = I.make_weights(model)
-    run = GpuRun(wl, w, model_id=42, max_tokens=256)
+    run = DeviceCase(wl, w, model_id=42, max_tokens=256)
     assert run.cache.model_id() == 42
     run.build([0, 1])
     assert run.cache.free_pages() == 0
