@@ -114,7 +114,9 @@ void tx_model_destroy(tx_model* model);
 #define TX_PAGE_TOKENS 64
 
 /* Bytes of one page: for each encoder layer then each decoder layer, K as
- * [H][64][d_head] and V transposed as [H][d_head][64]. */
+ * [H][64][d_head] and V transposed as [H][d_head][64], each V^T row holding
+ * the page's tokens in 16-token groups ordered 0-3, 8-11, 4-7, 12-15 (the k
+ * order of the attention MFMAs; tx_kv_cache_export returns plain order). */
 size_t tx_kv_page_bytes(const tx_config* cfg);
 
 /* Bytes of the device pool for n_pages pages plus the device page table of

@@ -37,19 +37,13 @@ struct MfmaAcc {
   }
 };
 
-// V^T tiles in LDS hold each 16-key group in the order 0-3, 8-11, 4-7, 12-15
-// (vt_pos maps a key to its column), so that the 8 keys one lane needs for a
-// PV fragment are contiguous.
-__device__ __forceinline__ int vt_pos(int key) {
-  return (key & ~15) | (key & 3) | ((key & 4) << 1) | ((key & 8) >> 1);
-}
-
 // One 64-key tile for one wave: S^T = K Q^T on MFMA (keys as rows, so lane
 // l32 + 32*hi holds 32 keys of query l32), online softmax update, then
 // O^T += V^T P^T with P^T taken from the S^T accumulators: the MFMA k index
 // 8*hi + t stands for key base + 8*(t/4) + 4*hi + t%4 on both operands, so no
-// register shuffle is needed, and the permuted V^T tile supplies exactly those
-// keys with one 16-byte LDS read.
+// register shuffle is needed, and a V^T tile held in the stored column order
+// (vt_col: 16-key groups as 0-3, 8-11, 4-7, 12-15) supplies exactly those keys
+// with one 16-byte LDS read.
 // The running max is kept in raw logit units, so scaling and max subtraction
 // fuse into one FMA before exp2. When `masked` (uniform across the wave) every
 // raw logit goes through `mask(key, s)`, which returns it (plus any bias, in
@@ -89,7 +83,8 @@ __device__ __forceinline__ void mfma_attend_tile(const bf16* __restrict__ sK, co
   const bool bump = mx > acc.m + 8.f / scale_log2;
   if (__any(bump)) {
     const float m_new = bump ? mx : acc.m;
-    const float alpha = __builtin_amdgcn_exp2f((acc.m - m_new) * scale_log2);  // 0 when acc.m = -inf
+    // 1 where the reference stays (also at -inf), 0 where it leaves -inf
+    const float alpha = bump ? __builtin_amdgcn_exp2f((acc.m - m_new) * scale_log2) : 1.f;
     acc.l *= alpha;
 #pragma unroll
     for (int db = 0; db < DH / 32; ++db)
@@ -144,16 +139,17 @@ __device__ __forceinline__ void mfma_store_out(const MfmaAcc<DH>& acc, bf16* __r
 //
 // A block of 4 waves serves up to 128 queries of one (request, head); each
 // wave owns 32 queries. For every 64-token page the block stages K [64][dh]
-// and V^T [dh][64] in LDS (double-buffered, the next page prefetched into
-// registers while the current one is used), so every K/V byte fetched from
-// HBM/L2 feeds all queries of the block.
+// and V^T [dh][64] in LDS (double-buffered; the next two pages travel from HBM
+// in registers while the current one is used), so every K/V byte fetched from
+// HBM/L2 feeds all queries of the block. The page keeps V^T in the column
+// order the PV MFMA wants, so both tiles go to LDS as plain 16-byte stores.
 //
 // Per wave and page:  S^T = K Q^T  (v_mfma_f32_32x32x16_bf16, keys as rows so
 // that a lane holds 32 keys of one query: the softmax row reduction is within
 // the lane plus one exchange with lane l^32), online softmax update, then
 // O^T += V^T P^T with P^T taken straight from the S^T accumulators (the MFMA
 // k index is permuted consistently on both operands, so no register shuffle
-// is needed; V^T supplies the matching keys with two 8-byte LDS reads).
+// is needed; V^T supplies the matching keys with one 16-byte LDS read).
 // Keys past the request's length are masked by selection and their V columns
 // are zeroed in LDS so that unused page slots (of any content) never reach
 // the output.
@@ -205,9 +201,13 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
   }
   const int32_t* ptab = page_table + (size_t)rq.slot * max_pages;
 
-  bf16x8 rk[NCH], rv[NCH];
-  auto gload = [&](int p) {
-    const size_t base = (size_t)ptab[p] * g.page_elems;
+  // Two register sets carry pages p+1 and p+2 from HBM while page p is used
+  // from LDS, so a load has two pages of compute to arrive.
+  bf16x8 ka[NCH], va[NCH], kb[NCH], vb[NCH];
+  auto gload = [&](int p, bf16x8 (&rk)[NCH], bf16x8 (&rv)[NCH]) {
+    // past the last page the last page is fetched again (unconditional loads
+    // keep the wait before each LDS store down to the older register set)
+    const size_t base = (size_t)ptab[min(p, n_pages - 1)] * g.page_elems;
     const bf16x8* kp = reinterpret_cast<const bf16x8*>(pool + base + g.k_off(layer_slot, h));
     const bf16x8* vp = reinterpret_cast<const bf16x8*>(pool + base + g.v_off(layer_slot, h));
 #pragma unroll
@@ -216,32 +216,26 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
       rv[u] = vp[tid + 256 * u];
     }
   };
-  auto lstore = [&](int buf, int p) {
+  auto lstore = [&](int buf, int p, const bf16x8 (&rk)[NCH], const bf16x8 (&rv)[NCH]) {
     const int valid = kv_len - p * kPage;  // keys of this page that exist (may exceed 64)
 #pragma unroll
     for (int u = 0; u < NCH; ++u) {
       const int e = (tid + 256 * u) * 8;
       *reinterpret_cast<bf16x8*>(&sK[buf][(e / DH) * KLD + (e % DH)]) = rk[u];
-      const int vr = e >> 6, vc = e & 63;  // V^T row (feature) and first key of the chunk
+      const int vr = e >> 6, vc = e & 63;  // V^T row (feature) and first stored column of the chunk
       bf16x8 vv = rv[u];
       if (valid < kPage) {  // only the request's last page is partial (uniform branch)
 #pragma unroll
         for (int t = 0; t < 8; ++t)
-          if (vc + t >= valid) vv[t] = (bf16)0.f;
+          if (vt_col(vc + t) >= valid) vv[t] = (bf16)0.f;
       }
-      // keys vc..vc+3 and vc+4..vc+7 land at their permuted columns
-      bf16* vrow = &sV[buf][vr * VLD];
-      *reinterpret_cast<bf16x4*>(vrow + vt_pos(vc)) = bf16x4{vv[0], vv[1], vv[2], vv[3]};
-      *reinterpret_cast<bf16x4*>(vrow + vt_pos(vc + 4)) = bf16x4{vv[4], vv[5], vv[6], vv[7]};
+      *reinterpret_cast<bf16x8*>(&sV[buf][vr * VLD + vc]) = vv;
     }
   };
-
-  gload(0);
-  lstore(0, 0);
-  __syncthreads();
-  for (int p = 0; p < n_pages; ++p) {
+  auto step = [&](int p, bf16x8 (&fk)[NCH], bf16x8 (&fv)[NCH], const bf16x8 (&nk)[NCH], const bf16x8 (&nv)[NCH]) {
+    // fk/fv held page p (already in LDS) and now take page p+2; nk/nv hold page p+1
     const int buf = p & 1;
-    if (p + 1 < n_pages) gload(p + 1);
+    gload(p + 2, fk, fv);
     if (wave_active) {
       const int key0 = p * kPage;
       // masking is needed on the request's last (partial) page and, when
@@ -259,8 +253,17 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
       };
       mfma_attend_tile<DH, KLD, VLD>(sK[buf], sV[buf], qf, acc, scale_log2, l32, hi, needs_mask, mask);
     }
-    if (p + 1 < n_pages) lstore(buf ^ 1, p + 1);
+    if (p + 1 < n_pages) lstore(buf ^ 1, p + 1, nk, nv);
     __syncthreads();
+  };
+
+  gload(0, ka, va);
+  gload(1, kb, vb);
+  lstore(0, 0, ka, va);
+  __syncthreads();
+  for (int p = 0; p < n_pages; p += 2) {
+    step(p, ka, va, kb, vb);
+    if (p + 1 < n_pages) step(p + 1, kb, vb, ka, va);
   }
   if (q_valid) mfma_store_out<DH>(acc, out + (size_t)row * ldo + h * DH, hi);
 }
@@ -333,7 +336,7 @@ __global__ __launch_bounds__(256, 2) void self_attn_mfma(const bf16* __restrict_
         }
         *reinterpret_cast<bf16x8*>(&sK[(k0 + w) * KLD + col]) = kv[w];
       }
-      const int vp = vt_pos(k0);
+      const int vp = vt_col(k0);
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
         typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -420,8 +423,8 @@ __global__ __launch_bounds__(256) void paged_attn_plain(const T* __restrict__ q,
     const int valid = min(kPage, kv_len - p * kPage);
     for (int e = tid; e < kPage * DH; e += 256) {
       sK[e / DH][e % DH] = (float)kp[e];
-      const int vr = e / kPage, vc = e % kPage;
-      sV[vr][vc] = vc < valid ? (float)vp[e] : 0.f;
+      const int vr = e / kPage, key = vt_col(e % kPage);
+      sV[vr][key] = key < valid ? (float)vp[e] : 0.f;
     }
     __syncthreads();
     if (active) {

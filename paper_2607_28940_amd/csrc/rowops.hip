@@ -152,7 +152,7 @@ __global__ __launch_bounds__(256) void scatter_kv(const T* __restrict__ src, int
 #pragma unroll
     for (int e = 0; e < 8; ++e) dst[e] = s[e];
   } else {
-    T* dst = base + g.v_off(slot0 + layer, h) + (size_t)(ch * 8) * kPage + t;
+    T* dst = base + g.v_off(slot0 + layer, h) + (size_t)(ch * 8) * kPage + vt_col(t);
 #pragma unroll
     for (int e = 0; e < 8; ++e) dst[(size_t)e * kPage] = s[e];
   }
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(256) void export_kv(const T* __restrict__ pool, con
   const int c = (int)(idx % d), h = c / g.dh, f = c % g.dh;
   const T* base = pool + (size_t)page_row[pos / kPage] * g.page_elems;
   const int t = (int)(pos % kPage);
-  out[idx] = is_v ? base[g.v_off(layer_slot, h) + (size_t)f * kPage + t] : base[g.k_off(layer_slot, h) + (size_t)t * g.dh + f];
+  out[idx] = is_v ? base[g.v_off(layer_slot, h) + (size_t)f * kPage + vt_col(t)] : base[g.k_off(layer_slot, h) + (size_t)t * g.dh + f];
 }
 
 hipError_t launch_export_kv(bool bf, const void* pool, const int32_t* page_row, PageGeom g, int layer_slot, int is_v,

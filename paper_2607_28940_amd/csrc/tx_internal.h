@@ -52,6 +52,11 @@ struct ScatterReq {
 
 // Geometry of a cache page: for each layer slot (encoder layers, then decoder
 // layers), K as [H][64][dh] then V transposed as [H][dh][64].
+// Column of token t (0..63 within its page) in a stored V^T row: every group
+// of 16 tokens is kept in the order 0-3, 8-11, 4-7, 12-15, the k order the
+// bf16 attention kernels feed to the PV MFMA (the map is its own inverse).
+__host__ __device__ inline int vt_col(int t) { return (t & ~15) | (t & 3) | ((t & 4) << 1) | ((t & 8) >> 1); }
+
 struct PageGeom {
   int32_t H, dh, n_slots;
   int64_t page_elems;  // elements per page
