@@ -64,6 +64,14 @@ __device__ __forceinline__ void mfma_attend_tile(const bf16* __restrict__ sK, co
       s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
     }
   }
+  // keep four K fragment reads in flight ahead of the MFMA that uses them
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+  for (int g = 0; g < DH / 8 - 4; ++g) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
   if (masked) {  // wave-uniform
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
