@@ -56,7 +56,8 @@ def _load(path: Optional[str] = None):
         lib.ox_encode_append.argtypes = [P(_Cfg), wp, dp, dp, ctypes.c_int, dp, ctypes.c_int, dp, dp, dp]
         lib.ox_cross_kv.argtypes = [P(_Cfg), wp, dp, ctypes.c_int, dp, dp]
         lib.ox_score.argtypes = [P(_Cfg), wp, dp, dp, ctypes.c_int, dp, ctypes.c_int, dp, ctypes.c_int, dp, dp, dp]
-        for f in ("ox_encode", "ox_encode_append", "ox_cross_kv", "ox_score"):
+        lib.ox_pool.argtypes = [ctypes.c_int, dp, ctypes.c_int, dp, dp]
+        for f in ("ox_encode", "ox_encode_append", "ox_cross_kv", "ox_score", "ox_pool"):
             getattr(lib, f).restype = None
         _libs[path] = lib
     return _libs[path]
@@ -74,7 +75,11 @@ def _f64(a) -> np.ndarray:
 
 
 class Oracle:
-    """One model (config + weights in canonical order) evaluated in fp64."""
+    """One model (config + weights in canonical order) evaluated in fp64.
+
+    A model with local-global sparse cross-attention (model.l_local > 0) has
+    one more tensor at the end of the list when model.global_pool is set: the
+    pooling vector w_pool [d]."""
 
     def __init__(self, model, weights: Sequence[np.ndarray], lib_path: Optional[str] = None):
         self.model = model
@@ -82,9 +87,12 @@ class Oracle:
         self.cfg = _Cfg(model.d_model, model.n_heads, model.d_ffn, model.n_enc_layers, model.n_dec_layers,
                         model.rel_pos_buckets, float(model.ln_eps))
         n = self.lib.ox_n_weights(ctypes.byref(self.cfg))
-        if n != len(weights):
-            raise ValueError(f"oracle expects {n} tensors, got {len(weights)}")
-        self._w = [_f64(w).reshape(-1) if np.asarray(w).size else np.zeros(1) for w in weights]
+        self.l_local = int(getattr(model, "l_local", 0))
+        has_pool = bool(getattr(model, "global_pool", False))
+        if n + has_pool != len(weights):
+            raise ValueError(f"oracle expects {n + has_pool} tensors, got {len(weights)}")
+        self.w_pool = _f64(weights[n]).reshape(-1) if has_pool else None
+        self._w = [_f64(w).reshape(-1) if np.asarray(w).size else np.zeros(1) for w in weights[:n]]
         self._wp = (ctypes.POINTER(ctypes.c_double) * n)(*[_dp(w) for w in self._w])
 
     @property
@@ -140,15 +148,38 @@ class Oracle:
             return out, tr, float(err[0])
         return out
 
+    def pool(self, Henc, w=None) -> np.ndarray:
+        """Attention-pooled global token of the encoded rows [L, d] -> [d]
+        (the model's pooling vector unless w is given)."""
+        Henc = _f64(Henc)
+        w = self.w_pool if w is None else _f64(w).reshape(-1)
+        g = np.empty(self.d)
+        self.lib.ox_pool(self.d, _dp(Henc), Henc.shape[0], _dp(w), _dp(g))
+        return g
+
+    def key_rows(self, Henc) -> np.ndarray:
+        """Encoded rows the decoder's cross-attention sees (Sec. 4.1.2): all of
+        them for dense cross-attention; for the local-global sparse form the
+        last l_local rows, followed by the pooled global token when the model
+        has one."""
+        Henc = _f64(Henc)
+        if self.l_local <= 0:
+            return Henc
+        rows = Henc[max(0, Henc.shape[0] - self.l_local):]
+        if self.w_pool is not None:
+            rows = np.concatenate([rows, self.pool(Henc)[None, :]], 0)
+        return rows
+
     def run_request(self, Xb, Xs, Xc, Xev=None):
         """Whole path for one request: encode behavior (then append events if
-        given), project cross K/V, decode, score. Returns (scores, state dict)."""
+        given), project cross K/V of the rows the cross-attention sees, decode,
+        score. Returns (scores, state dict)."""
         H, K, V, _ = self.encode(Xb)
         if Xev is not None and len(Xev):
             Hn, Kn, Vn = self.encode_append(K, V, Xev)
             H = np.concatenate([H, Hn], 0)
             K = np.concatenate([K, Kn], 1)
             V = np.concatenate([V, Vn], 1)
-        Kx, Vx = self.cross_kv(H)
+        Kx, Vx = self.cross_kv(self.key_rows(H))
         s = self.score(Kx, Vx, Xs, Xc)
         return s, {"H": H, "K": K, "V": V, "Kx": Kx, "Vx": Vx}

@@ -22,7 +22,14 @@
  *     Eq. action-decoding),
  *   - incremental append: only the new tokens are encoded, against the stored
  *     per-layer keys/values of the prefix (App. D, remark on incremental
- *     encoding; Sec. 4.2, causal attention and prefix reuse).
+ *     encoding; Sec. 4.2, causal attention and prefix reuse),
+ *   - the global anchor token of the local-global sparse cross-attention: an
+ *     attention pooling of the encoder output (Sec. 4.1.2, paragraph on
+ *     local-global sparse cross attention; Sec. 5 setup, "attention pooling to
+ *     generate the global token"). The sparse variant itself needs no code of
+ *     its own: the decoder's cross-attention is evaluated over the restricted
+ *     key set (the last L_local cached tokens plus the pooled token), which the
+ *     caller passes in place of the full cache.
  *
  * Readings where the paper is silent or ambiguous:
  *   - decoder sublayer order self -> cross -> FFN, separate softmaxes,
@@ -33,7 +40,11 @@
  *   - relative bias beta_h[min(i - j, R - 1)] added to encoder logits, R = 0
  *     disables it; the decoder has no position term,
  *   - every projection has a bias; y = x W with W stored [d_in, d_out]; head h
- *     owns columns h*d_h .. h*d_h + d_h - 1.
+ *     owns columns h*d_h .. h*d_h + d_h - 1,
+ *   - attention pooling: one learned vector w, weights softmax_j(h_j . w /
+ *     sqrt(d)) over all encoded rows, pooled token sum_j weight_j h_j; its
+ *     keys/values come from the same cross-attention projections as any
+ *     cached row.
  *
  * Everything is double precision, evaluated in the order the definitions
  * state. OpenMP only splits independent rows / (head, query) pairs.
@@ -341,4 +352,29 @@ void ox_score(const ox_cfg* c, const double* const* W, const double* Kx, const d
   free(P);
   free(T1);
   free(T2);
+}
+
+/*
+ * Attention pooling of the encoded behavior rows: the global anchor token of
+ * the local-global sparse cross-attention (Sec. 4.1.2; Sec. 5 setup).
+ *   Henc [L][d], w [d] -> g [d],  g = sum_j a_j h_j,
+ *   a = softmax over j of (h_j . w / sqrt(d)).
+ */
+void ox_pool(int d, const double* Henc, int L, const double* w, double* g) {
+  double* z = (double*)malloc(sizeof(double) * (size_t)(L > 0 ? L : 1));
+  double mx = -INFINITY;
+  for (int j = 0; j < L; ++j) {
+    double s = 0.0;
+    for (int k = 0; k < d; ++k) s += Henc[(size_t)j * d + k] * w[k];
+    z[j] = s / sqrt((double)d);
+    if (z[j] > mx) mx = z[j];
+  }
+  double den = 0.0;
+  for (int j = 0; j < L; ++j) den += exp(z[j] - mx);
+  for (int k = 0; k < d; ++k) g[k] = 0.0;
+  for (int j = 0; j < L; ++j) {
+    const double a = exp(z[j] - mx) / den;
+    for (int k = 0; k < d; ++k) g[k] += a * Henc[(size_t)j * d + k];
+  }
+  free(z);
 }

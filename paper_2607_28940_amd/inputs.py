@@ -47,6 +47,11 @@ class ModelConfig:
     rel_pos_buckets: int = 128
     ln_eps: float = 1e-5
     dtype: str = "bf16"  # "bf16" or "f32": storage type of inputs, weights, cache, activations
+    # local-global sparse cross-attention (Sec. 4.1.2): 0 = every cached token;
+    # L > 0 = the last L cached tokens, plus the attention-pooled global token
+    # when global_pool is set
+    l_local: int = 0
+    global_pool: bool = False
 
     @property
     def d_head(self) -> int:
@@ -101,11 +106,13 @@ def weight_specs(m: ModelConfig) -> List[tuple]:
             out.append(("dec", l, n, shp))
     out.append(("head", 0, "w_s", (d,)))
     out.append(("head", 0, "b_s", (1,)))
+    if m.global_pool:
+        out.append(("pool", 0, "w_pool", (d,)))
     return out
 
 
 def n_weights(m: ModelConfig) -> int:
-    return 17 * m.n_enc_layers + 26 * m.n_dec_layers + 2
+    return 17 * m.n_enc_layers + 26 * m.n_dec_layers + 2 + int(bool(m.global_pool))
 
 
 def _round_storage(x: np.ndarray, dtype: str) -> np.ndarray:
@@ -133,6 +140,8 @@ def make_weights(m: ModelConfig, variant: Sequence[str] = (), seed_w: int = SEED
       relative-position table ~ N(0, 1), so attention logits have std of a few
       units and softmax is far from uniform.
     variant "affine": LayerNorm gain 1 + N(0, 0.1), offset N(0, 0.1).
+    The pooling vector of the global token is N(0, 0.02) (nearly uniform
+    pooling), N(0, 16) under "sharp" (pooling logits of a few units).
     """
     variant = set(variant)
     d = m.d_model
@@ -146,6 +155,8 @@ def make_weights(m: ModelConfig, variant: Sequence[str] = (), seed_w: int = SEED
             w = 0.1 * z if "affine" in variant else 0.0 * z
         elif name == "rel":
             w = (1.0 if "sharp" in variant else 0.02) * z
+        elif name == "w_pool":
+            w = (4.0 if "sharp" in variant else 0.02) * z
         elif "sharp" in variant and name in ("Wq", "Wk", "sWq", "sWk", "xWq", "xWk"):
             w = (2.0 / math.sqrt(d)) * z
         else:

@@ -7,7 +7,9 @@ dropout 0 and activation "gelu" are the textbook post-LN blocks
 The relative-position bias enters through a per-head additive float mask; the
 candidate-isolating decoder mask (App. B) through a boolean mask. None of this
 code is shared with the oracle: the projections, softmax, LayerNorm and GELU
-are PyTorch's.
+are PyTorch's. For the local-global sparse cross-attention the decoder's
+memory is the last l_local encoded rows plus the pooled global token
+(torch.softmax over h_j . w / sqrt(d), then a weighted sum of the rows).
 """
 from __future__ import annotations
 
@@ -31,7 +33,8 @@ def _split(m: ModelConfig, weights):
         dec.append(dict(zip(DEC_NAMES, weights[i:i + len(DEC_NAMES)])))
         i += len(DEC_NAMES)
     head = (weights[i], weights[i + 1])
-    return enc, dec, head
+    pool = weights[i + 2] if m.global_pool else None
+    return enc, dec, head, pool
 
 
 def _set_mha(mha: torch.nn.MultiheadAttention, Wq, bq, Wk, bk, Wv, bv, Wo, bo):
@@ -45,7 +48,8 @@ def _set_mha(mha: torch.nn.MultiheadAttention, Wq, bq, Wk, bk, Wv, bv, Wo, bo):
 class TorchTransX:
     def __init__(self, m: ModelConfig, weights):
         self.m = m
-        enc, dec, head = _split(m, weights)
+        enc, dec, head, pool = _split(m, weights)
+        self.w_pool = None if pool is None else _t(pool).reshape(-1)
         d, H, F = m.d_model, m.n_heads, m.d_ffn
         kw = dict(dropout=0.0, activation="gelu", batch_first=True, norm_first=False, dtype=torch.float64)
         self.enc_layers = []
@@ -127,6 +131,18 @@ class TorchTransX:
         z = t[0, S:].detach()
         return (z @ self.w_s + self.b_s).numpy()
 
+    def memory(self, Henc) -> torch.Tensor:
+        """Rows the cross-attention attends to: all encoded rows, or the
+        local-global sparse set."""
+        Henc = _t(Henc)
+        if self.m.l_local <= 0:
+            return Henc
+        rows = Henc[max(0, Henc.shape[0] - self.m.l_local):]
+        if self.w_pool is not None:
+            a = torch.softmax(Henc @ self.w_pool / float(np.sqrt(self.m.d_model)), 0)
+            rows = torch.cat([rows, (a @ Henc)[None]], 0)
+        return rows
+
     def run_request(self, Xb, Xs, Xc, Xev=None) -> np.ndarray:
         X = Xb if Xev is None else np.concatenate([Xb, Xev], 0)
-        return self.score(self.encode(X), Xs, Xc)
+        return self.score(self.memory(self.encode(X)), Xs, Xc)
