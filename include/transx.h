@@ -65,6 +65,16 @@ typedef struct {
   int32_t rel_pos_buckets; /* R: logit bias beta_h[min(i - j, R - 1)]; 0 = none */
   float ln_eps;
   int32_t dtype;           /* tx_dtype */
+  /* Local-global sparse cross-attention (Sec. 4.1.2, Eq. sparse-cross-attn;
+   * the experiments use L_local = 10 with an attention-pooled global token,
+   * Sec. 5 setup). l_local = 0: every decoder query attends to every cached
+   * token. 1 <= l_local <= 64: only to the request's last l_local cached
+   * tokens, plus, when global_pool = 1, one global anchor token: the
+   * attention pooling g = sum_j a_j h_j of the encoded rows with
+   * a = softmax_j(h_j . w_pool / sqrt(d_model)), projected by each decoder
+   * layer's cross-attention K/V weights. global_pool requires l_local > 0. */
+  int32_t l_local;
+  int32_t global_pool;
 } tx_config;
 
 typedef struct tx_model tx_model;
@@ -81,6 +91,7 @@ const char* tx_last_error(void);
  *                           cross Wq bq Wk bk Wv bv Wo bo ln2_g ln2_b,
  *                           FFN W1 b1 W2 b2 ln3_g ln3_b
  *   head (2): w_s[d] b_s[1]
+ *   global-token pooling (1, only when global_pool): w_pool[d]
  * Matrices are [d_in][d_out] row-major (a layer computes y = x W + b). */
 int32_t tx_num_weights(const tx_config* cfg);
 
@@ -120,7 +131,9 @@ void tx_model_destroy(tx_model* model);
 size_t tx_kv_page_bytes(const tx_config* cfg);
 
 /* Bytes of the device pool for n_pages pages plus the device page table of
- * max_requests requests of up to max_tokens tokens each. */
+ * max_requests requests of up to max_tokens tokens each; with global_pool
+ * also, per request, the pooling state (fp32 max, sum and weighted row sum)
+ * and the global token's cross-attention K/V of every decoder layer. */
 size_t tx_kv_pool_bytes(const tx_config* cfg, int64_t n_pages, int32_t max_requests, int64_t max_tokens);
 
 /* Create a cache over a caller-owned device pool (256-byte aligned). Request
@@ -145,7 +158,9 @@ uint64_t tx_kv_cache_model_id(const tx_kv_cache* cache);
 /* Copy one cached tensor of a request into a dense device buffer out
  * [len][d_model] (model dtype), head h in columns h*d_head .. h*d_head+d_head-1.
  * part: 0 encoder K, 1 encoder V (layer < n_enc), 2 cross-attention K,
- * 3 cross-attention V (layer < n_dec). For inspection and tests. */
+ * 3 cross-attention V (layer < n_dec); with global_pool, 4 and 5 are the
+ * global token's cross-attention K and V of decoder layer `layer` (one row).
+ * For inspection and tests. */
 int tx_kv_cache_export(const tx_kv_cache* cache, int32_t req_id, int32_t part, int32_t layer, void* out,
                        hipStream_t stream);
 

@@ -94,6 +94,9 @@ struct tx_model {
   Mat xkv;  // cross-attention K and V of every decoder layer: [n_dec * 2d][d]
   float* ws;
   float* bs;
+  float* wpool = nullptr;  // attention-pooling vector of the global token [d]
+  int l_local = 0;         // > 0: local-global sparse cross-attention
+  bool gpool = false;      // the sparse key set includes the pooled global token
   bool weights_set = false;
 };
 
@@ -109,6 +112,11 @@ static int check_config(const tx_config* c) {
     return fail(TX_E_INVALID, "layer counts enc %d dec %d", c->n_enc_layers, c->n_dec_layers);
   if (c->rel_pos_buckets < 0) return fail(TX_E_INVALID, "rel_pos_buckets %d", c->rel_pos_buckets);
   if (!(c->ln_eps > 0.f)) return fail(TX_E_INVALID, "ln_eps must be positive");
+  if (c->l_local < 0) return fail(TX_E_INVALID, "l_local %d", c->l_local);
+  if (c->l_local > kMaxLocal) return fail(TX_E_UNSUPPORTED, "l_local %d above %d", c->l_local, kMaxLocal);
+  if (c->global_pool != 0 && c->global_pool != 1) return fail(TX_E_INVALID, "global_pool %d", c->global_pool);
+  if (c->global_pool && c->l_local == 0)
+    return fail(TX_E_INVALID, "the pooled global token belongs to the sparse cross-attention (l_local > 0)");
   return TX_OK;
 }
 
@@ -146,6 +154,7 @@ static void layout_model(const tx_config& c, Carver& cv, tx_model& m) {
   m.xkv = mat(2 * d * c.n_dec_layers, d);
   m.ws = vec(d);
   m.bs = vec(1);
+  if (c.global_pool) m.wpool = vec(d);
 }
 
 extern "C" {
@@ -154,7 +163,7 @@ const char* tx_last_error(void) { return g_err.c_str(); }
 
 int32_t tx_num_weights(const tx_config* cfg) {
   if (!cfg) return -1;
-  return E_N * cfg->n_enc_layers + D_N * cfg->n_dec_layers + 2;
+  return E_N * cfg->n_enc_layers + D_N * cfg->n_dec_layers + 2 + (cfg->global_pool ? 1 : 0);
 }
 
 size_t tx_model_repack_bytes(const tx_config* cfg) {
@@ -184,6 +193,8 @@ int tx_model_create(const tx_config* cfg, void* dev_repack, size_t repack_bytes,
   m->n_dec = cfg->n_dec_layers;
   m->R = cfg->rel_pos_buckets;
   m->esz = m->bf ? 2 : 4;
+  m->l_local = cfg->l_local;
+  m->gpool = cfg->global_pool != 0;
   Carver cv(dev_repack);
   layout_model(*cfg, cv, *m);
   *out = m;
@@ -264,6 +275,7 @@ int tx_model_set_weights(tx_model* m, const void* const* W, int32_t n_weights, h
   const int hb = E_N * m->n_enc + D_N * m->n_dec;
   run(bias(hb, m->ws, d));
   run(bias(hb + 1, m->bs, 1));
+  if (m->gpool) run(bias(hb + 2, m->wpool, d));
   if (e != hipSuccess) return fail(TX_E_HIP, "weight repack launch failed: %s", hipGetErrorString(e));
   m->weights_set = true;
   return TX_OK;
@@ -344,6 +356,12 @@ struct tx_kv_cache {
   size_t page_bytes;
   PageGeom geom;
   int32_t* d_table;  // device [max_req][max_pages]
+  // global token of the sparse cross-attention, per page-table row: pooling
+  // state (max, sum) and weighted row sum (fp32), and its cross K/V rows
+  // [n_dec * 2d] in the model dtype (layer l: K at 2l*d, V at (2l+1)*d)
+  float* d_pool_ml = nullptr;
+  float* d_pool_acc = nullptr;
+  char* d_gkv = nullptr;
   std::vector<int32_t> h_table;
   std::vector<std::vector<int32_t>> pages;
   std::vector<int64_t> len;  // -1: no cache
@@ -359,10 +377,19 @@ size_t tx_kv_page_bytes(const tx_config* c) {
   return (size_t)(c->n_enc_layers + c->n_dec_layers) * 2 * kPage * c->d_model * es;
 }
 
+// Bytes of the per-request global-token records that follow the page table.
+static size_t global_token_bytes(const tx_config* c, int64_t max_requests) {
+  if (!c->global_pool) return 0;
+  const size_t es = c->dtype == TX_BF16 ? 2 : 4, d = c->d_model;
+  return align_up((size_t)max_requests * 2 * 4) + align_up((size_t)max_requests * d * 4) +
+         align_up((size_t)max_requests * 2 * c->n_dec_layers * d * es);
+}
+
 size_t tx_kv_pool_bytes(const tx_config* c, int64_t n_pages, int32_t max_requests, int64_t max_tokens) {
   if (check_config(c) != TX_OK || n_pages < 0 || max_requests < 0 || max_tokens < 0) return 0;
   const int64_t mp = (max_tokens + kPage - 1) / kPage;
-  return align_up((size_t)n_pages * tx_kv_page_bytes(c)) + align_up((size_t)max_requests * mp * 4);
+  return align_up((size_t)n_pages * tx_kv_page_bytes(c)) + align_up((size_t)max_requests * mp * 4) +
+         global_token_bytes(c, max_requests);
 }
 
 int tx_kv_cache_create(const tx_model* m, void* dev_pool, size_t pool_bytes, int64_t n_pages, int32_t max_requests,
@@ -390,6 +417,14 @@ int tx_kv_cache_create(const tx_model* m, void* dev_pool, size_t pool_bytes, int
   c->geom.n_slots = m->n_enc + m->n_dec;
   c->geom.page_elems = (int64_t)(c->page_bytes / m->esz);
   c->d_table = (int32_t*)(c->pool + align_up((size_t)n_pages * c->page_bytes));
+  if (m->gpool) {
+    char* p = (char*)c->d_table + align_up((size_t)max_requests * c->max_pages * 4);
+    c->d_pool_ml = (float*)p;
+    p += align_up((size_t)max_requests * 2 * 4);
+    c->d_pool_acc = (float*)p;
+    p += align_up((size_t)max_requests * m->d * 4);
+    c->d_gkv = p;
+  }
   c->h_table.assign((size_t)max_requests * c->max_pages, 0);
   c->pages.resize(max_requests);
   c->len.assign(max_requests, -1);
@@ -430,7 +465,15 @@ int tx_kv_cache_export(const tx_kv_cache* c, int32_t id, int32_t part, int32_t l
   if (!c || !out) return fail(TX_E_INVALID, "null argument");
   if (id < 0 || id >= c->max_req) return fail(TX_E_INVALID, "request id %d out of range", id);
   if (c->len[id] < 0) return fail(TX_E_NOCACHE, "request %d has no cache", id);
-  if (part < 0 || part > 3) return fail(TX_E_INVALID, "part %d", part);
+  if (part < 0 || part > 5) return fail(TX_E_INVALID, "part %d", part);
+  if (part >= 4) {  // the global token's cross-attention key (4) or value (5)
+    if (!c->m->gpool) return fail(TX_E_INVALID, "model has no pooled global token");
+    if (layer < 0 || layer >= c->m->n_dec) return fail(TX_E_INVALID, "layer %d", layer);
+    const size_t es = c->m->esz, d = c->m->d;
+    const char* src = c->d_gkv + ((size_t)id * 2 * c->m->n_dec * d + (size_t)(2 * layer + (part - 4)) * d) * es;
+    TX_HIP(hipMemcpyAsync(out, src, d * es, hipMemcpyDeviceToDevice, stream));
+    return TX_OK;
+  }
   if (c->len[id] == 0) return TX_OK;
   const int nl = part < 2 ? c->m->n_enc : c->m->n_dec;
   if (layer < 0 || layer >= nl) return fail(TX_E_INVALID, "layer %d", layer);
@@ -447,13 +490,13 @@ int tx_kv_cache_export(const tx_kv_cache* c, int32_t id, int32_t part, int32_t l
 namespace {
 enum KClass {
   K_GEMM_QKV, K_GEMM_O, K_GEMM_XQ, K_GEMM_XO, K_GEMM_FFN1, K_GEMM_FFN2, K_SELF_ATTN, K_CROSS_ATTN, K_LAYERNORM,
-  K_LN_SCORE, K_COPY, K_ENC_GEMM, K_ENC_ATTN, K_ENC_LAYERNORM, K_SCATTER, K_XKV_GEMM, K_COUNT
+  K_LN_SCORE, K_COPY, K_ENC_GEMM, K_ENC_ATTN, K_ENC_LAYERNORM, K_SCATTER, K_XKV_GEMM, K_POOL, K_COUNT
 };
 const char* const kClassNames[K_COUNT] = {
     "score.gemm_qkv", "score.gemm_self_out", "score.gemm_cross_q", "score.gemm_cross_out", "score.gemm_ffn_up",
     "score.gemm_ffn_down", "score.self_attention", "score.cross_attention", "score.layernorm", "score.layernorm_score",
     "score.input_copy", "encode.gemm", "encode.causal_attention", "encode.layernorm", "encode.scatter_kv",
-    "encode.gemm_cross_kv"};
+    "encode.gemm_cross_kv", "encode.global_pool"};
 
 // Records a HIP event pair around each launch on the launching stream while
 // enabled; totals are folded in when read.
@@ -574,7 +617,9 @@ struct Meta {
 // Generous upper bound of a pass's metadata bytes.
 size_t meta_bound(int n_req, int64_t rows, int64_t max_rows, int H) {
   const int64_t tiles = (int64_t)H * (rows / 32 + n_req + 1) + 8 * (max_rows / 32 + 2);
-  return align_up(8192 + (size_t)n_req * 160 + (size_t)tiles * sizeof(AttnTile) * 6);
+  const int64_t pool_chunks = rows / 64 + n_req + 1;
+  return align_up(8192 + (size_t)n_req * 160 + (size_t)tiles * sizeof(AttnTile) * 6 +
+                  (size_t)pool_chunks * sizeof(PoolChunk) + (size_t)n_req * sizeof(PoolReq));
 }
 
 // Attention worklist: tiles of q_block queries for every (request, head),
@@ -657,8 +702,18 @@ size_t row_bytes(const tx_model* m, int op) {
   return m->esz * (d + 3 * d + d + d + std::max(F, (size_t)(2 * m->n_dec) * d));
 }
 
+// Workspace of the global-token pooling in an encoder pass: chunk partial
+// states, the pooled tokens and their cross K/V rows.
+size_t pool_pass_bytes(const tx_model* m, int op, int n, int64_t rows) {
+  if (!m->gpool || op == TX_OP_SCORE) return 0;
+  const size_t d = m->d;
+  return align_up((size_t)(rows / 64 + n + 1) * (d + 2) * 4) + align_up((size_t)n * d * m->esz) +
+         align_up((size_t)n * 2 * m->n_dec * d * m->esz) + 3 * 256;
+}
+
 size_t pass_bytes(const tx_model* m, int op, int n, int64_t rows, int64_t max_rows) {
-  return meta_bound(n, rows, max_rows, m->H) + align_up(rows * row_bytes(m, op)) + 6 * 256;
+  return meta_bound(n, rows, max_rows, m->H) + align_up(rows * row_bytes(m, op)) + 6 * 256 +
+         pool_pass_bytes(m, op, n, rows);
 }
 
 // rows of request i for the op
@@ -742,8 +797,20 @@ int run_encoder_pass(tx_kv_cache* c, const char* X, int64_t rows, const std::vec
   }
   std::vector<AttnTile> tiles;
   attn_tiles(areqs, m->H, qb, true, tiles);
+  // global-token pooling: 64-row chunks of each request's new rows
+  std::vector<PoolChunk> chunks;
+  std::vector<PoolReq> preqs;
+  if (m->gpool) {
+    for (int i = 0; i < n; ++i) {
+      const ScatterReq& s = sreqs[i];
+      const int c0 = (int)chunks.size();
+      for (int r = 0; r < s.n; r += 64) chunks.push_back({i, s.row0 + r, std::min(64, s.n - r), 0});
+      preqs.push_back({c0, (int)chunks.size() - c0, s.slot, s.pos0 == 0 ? 1 : 0});
+    }
+  }
   Meta meta;
   const size_t o_sreq = meta.put(sreqs), o_areq = meta.put(areqs), o_tiles = meta.put(tiles);
+  const size_t o_chunks = meta.put(chunks), o_preqs = meta.put(preqs);
   const size_t mb = meta_bound(n, rows, mx, m->H);
   if (meta.buf.size() > mb) return fail(TX_E_NOMEM, "internal: metadata %zu > bound %zu", meta.buf.size(), mb);
   TX_HIP(c->st.upload(ws, meta.buf.data(), meta.buf.size(), st));
@@ -757,6 +824,13 @@ int run_encoder_pass(tx_kv_cache* c, const char* X, int64_t rows, const std::vec
   char* A = cv.take<char*>(rows * d * es);
   char* Y = cv.take<char*>(rows * d * es);
   char* Hf = cv.take<char*>(rows * std::max(F, 2 * m->n_dec * d) * es);
+  float* pool_part = nullptr;
+  char *gtok = nullptr, *gkv_rows = nullptr;
+  if (m->gpool) {
+    pool_part = cv.take<float*>(chunks.size() * (size_t)(d + 2) * 4);
+    gtok = cv.take<char*>((size_t)n * d * es);
+    gkv_rows = cv.take<char*>((size_t)n * 2 * m->n_dec * d * es);
+  }
   const int M = (int)rows;
   const double dd = d, Md = (double)M, esd = (double)es;
   double attn_pairs = 0.0, kv_bytes = 0.0;
@@ -795,6 +869,18 @@ int run_encoder_pass(tx_kv_cache* c, const char* X, int64_t rows, const std::vec
   TX_LAUNCH(K_SCATTER, 0, 2 * Md * nkv * esd,
             launch_scatter_kv(bf, Hf, nkv, m->n_dec, m->n_enc, c->pool, c->d_table, c->max_pages, c->geom, d_sreq, n,
                               M, st));
+  if (m->gpool) {
+    // fold the new rows into each request's pooling state, then project the
+    // pooled token with every decoder layer's cross K/V weights
+    const PoolReq* d_preqs = (const PoolReq*)(ws + o_preqs);
+    const double nd = n;
+    TX_LAUNCH(K_POOL, 4 * Md * dd, 2 * Md * dd * esd,
+              launch_pool(bf, T, d, m->wpool, 1.f / sqrtf((float)d), (const PoolChunk*)(ws + o_chunks),
+                          (int)chunks.size(), d_preqs, n, pool_part, c->d_pool_ml, c->d_pool_acc, gtok, st));
+    TX_LAUNCH(K_POOL, 2 * nd * nkv * dd, esd * (nd * dd + nkv * dd + nd * nkv),
+              launch_gemm(bf, gtok, d, m->xkv.w, m->xkv.b, nullptr, 0, gkv_rows, nkv, n, nkv, d, EPI_BIAS, st));
+    TX_LAUNCH(K_POOL, 0, 2 * nd * nkv * esd, launch_store_rows(bf, gkv_rows, nkv, d_preqs, n, c->d_gkv, st));
+  }
   return TX_OK;
 }
 
@@ -950,7 +1036,9 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, int a, int b, const
     cand[i] = AttnReq{c_row, C, 0, 0, kv, 0, ids[r], 0};
     mx = std::max<int64_t>(mx, S + C);
   }
-  const int qb = paged_attention_q_block(bf, m->dh), sqb = self_attention_q_block(bf, m->dh);
+  const bool sparse = m->l_local > 0;
+  const int qb = sparse ? kLgQueryBlock : paged_attention_q_block(bf, m->dh);
+  const int sqb = self_attention_q_block(bf, m->dh);
   std::vector<AttnTile> t_full, t_cand;
   std::vector<SelfTile> s_full, s_cand;
   if (m->n_dec > 1) {
@@ -985,7 +1073,9 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, int a, int b, const
   // algorithmic work of the attention launches: (query, key) pairs and cache bytes
   double pairs_full = 0, pairs_cand = 0, self_full = 0, self_cand = 0, kvb = 0;
   for (int i = 0; i < n; ++i) {
-    const double S = sreq[i].S, C = sreq[i].C, kv = full[i].kv_len;
+    const double S = sreq[i].S, C = sreq[i].C;
+    // keys per query: the whole cache, or the sparse set
+    const double kv = sparse ? std::min(full[i].kv_len, m->l_local) + (m->gpool ? 1 : 0) : full[i].kv_len;
     pairs_full += (S + C) * kv;
     pairs_cand += C * kv;
     self_full += 0.5 * S * (S + 1) + C * (S + 1);
@@ -1020,8 +1110,11 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, int a, int b, const
     TX_LAUNCH(K_GEMM_XQ, xq.first, xq.second,
               launch_gemm(bf, T + ro, d, L.xq.w, L.xq.b, nullptr, 0, A + ro, d, Mr, d, d, EPI_BIAS, st));
     TX_LAUNCH(K_CROSS_ATTN, 4 * dd * (last ? pairs_cand : pairs_full), kvb + 2 * Mrd * dd * esd,
-              launch_paged_attention(bf, A, d, O, d, c->pool, c->d_table, c->max_pages, c->geom, m->n_enc + l, areq,
-                                     at, n_at, false, nullptr, 0, qb, st));
+              sparse ? launch_lg_attention(bf, A, d, O, d, c->pool, c->d_table, c->max_pages, c->geom, m->n_enc + l,
+                                           areq, at, n_at, m->l_local, m->gpool ? c->d_gkv : nullptr,
+                                           2 * m->n_dec * d, l, st)
+                     : launch_paged_attention(bf, A, d, O, d, c->pool, c->d_table, c->max_pages, c->geom,
+                                              m->n_enc + l, areq, at, n_at, false, nullptr, 0, qb, st));
     TX_LAUNCH(K_GEMM_XO, xo.first, xo.second,
               launch_gemm(bf, O + ro, d, L.xo.w, L.xo.b, T + ro, d, Y + ro, d, Mr, d, d, EPI_BIAS_RESID, st));
     TX_LAUNCH(K_LAYERNORM, 0, 2 * Mrd * dd * esd, launch_layernorm(bf, Y + ro, T + ro, L.ln2g, L.ln2b, Mr, d, eps, st));

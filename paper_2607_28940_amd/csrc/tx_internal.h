@@ -50,6 +50,19 @@ struct ScatterReq {
   int32_t row0, n, pos0, slot;
 };
 
+// Attention pooling work: rows row0 .. row0+n-1 (n <= 64) of the encoded
+// matrix, one chunk of the request at index `req` of the pass.
+struct PoolChunk {
+  int32_t req, row0, n, pad;
+};
+// Per request of a pass: its chunks chunk0 .. chunk0+n_chunks-1, its page-table
+// row (which also indexes the per-request pooling state and global-token K/V),
+// and whether the pooling starts afresh (build) or continues the stored state
+// (append).
+struct PoolReq {
+  int32_t chunk0, n_chunks, slot, fresh;
+};
+
 // Geometry of a cache page: for each layer slot (encoder layers, then decoder
 // layers), K as [H][64][dh] then V transposed as [H][dh][64].
 // Column of token t (0..63 within its page) in a stored V^T row: every group
@@ -108,6 +121,31 @@ hipError_t launch_scatter_kv(bool bf, const void* src, int lds, int n_layers, in
 // [len][H*dh] matrix.
 hipError_t launch_export_kv(bool bf, const void* pool, const int32_t* page_row, PageGeom g, int layer_slot, int is_v,
                             int64_t len, void* out, hipStream_t s);
+
+// Attention pooling of encoded rows H [rows][d] with vector w (fp32 [d]):
+// per chunk the running max, sum and weighted row sum of exp(h.w*zscale)
+// (part: fp32 [n_chunks][d + 2] = max, sum, acc[d]), then per request the
+// merge of its chunks with the stored state (ml: fp32 [max_req][2], acc:
+// fp32 [max_req][d]), which is updated in place, and the pooled token
+// acc / sum written to g_out [n_req][d] in the model's element type.
+hipError_t launch_pool(bool bf, const void* H, int d, const float* w, float zscale, const PoolChunk* chunks,
+                       int n_chunks, const PoolReq* reqs, int n_req, float* part, float* ml, float* acc, void* g_out,
+                       hipStream_t s);
+// dst[slot][0 .. W) = src[i][0 .. W) for every request i of the pass
+hipError_t launch_store_rows(bool bf, const void* src, int W, const PoolReq* reqs, int n_req, void* dst,
+                             hipStream_t s);
+// Local-global sparse cross-attention: each query attends to the last
+// min(l_local, kv_len) cached tokens of its request (layer slot layer_slot)
+// and, when gkv is not null, to the request's global token, whose key and
+// value are columns [2*dec_layer*d + h*dh ..) and [(2*dec_layer+1)*d + h*dh ..)
+// of row `slot` of gkv (row stride gkv_ld). Tiles of lg_attention_q_block()
+// queries.
+hipError_t launch_lg_attention(bool bf, const void* q, int ldq, void* out, int ldo, const void* pool,
+                               const int32_t* page_table, int max_pages, PageGeom g, int layer_slot,
+                               const AttnReq* reqs, const AttnTile* tiles, int n_tiles, int l_local,
+                               const void* gkv, int gkv_ld, int dec_layer, hipStream_t s);
+constexpr int kLgQueryBlock = 64;
+constexpr int kMaxLocal = 64;  // largest supported l_local
 
 // dst[n][k] = src[k][n] (src [K][N] row-major), same element type
 hipError_t launch_transpose(bool bf, const void* src, void* dst, int K, int N, int dst_ld, hipStream_t s);

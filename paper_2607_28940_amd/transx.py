@@ -39,12 +39,14 @@ class TxError(RuntimeError):
 class Config(ctypes.Structure):
     _fields_ = [("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("d_ffn", ctypes.c_int32),
                 ("n_enc_layers", ctypes.c_int32), ("n_dec_layers", ctypes.c_int32),
-                ("rel_pos_buckets", ctypes.c_int32), ("ln_eps", ctypes.c_float), ("dtype", ctypes.c_int32)]
+                ("rel_pos_buckets", ctypes.c_int32), ("ln_eps", ctypes.c_float), ("dtype", ctypes.c_int32),
+                ("l_local", ctypes.c_int32), ("global_pool", ctypes.c_int32)]
 
     @classmethod
     def of(cls, m: ModelConfig) -> "Config":
         return cls(m.d_model, m.n_heads, m.d_ffn, m.n_enc_layers, m.n_dec_layers, m.rel_pos_buckets,
-                   float(m.ln_eps), TX_BF16 if m.dtype == "bf16" else TX_F32)
+                   float(m.ln_eps), TX_BF16 if m.dtype == "bf16" else TX_F32, int(m.l_local),
+                   int(bool(m.global_pool)))
 
 
 _lib = None
@@ -259,9 +261,10 @@ class KVCache:
 
     def export(self, req_id: int, part: int, layer: int, stream=None):
         """Cached tensor of a request as a dense [len, d] device tensor.
-        part: 0 encoder K, 1 encoder V, 2 cross K, 3 cross V."""
+        part: 0 encoder K, 1 encoder V, 2 cross K, 3 cross V; 4 and 5 the
+        global token's cross K and V (one row) of a model with global pooling."""
         import torch
-        n = self.length(req_id)
+        n = 1 if part >= 4 else self.length(req_id)
         out = torch.empty((max(n, 0), self.model.mc.d_model), dtype=_torch_dtype(self.model.mc), device=self.device)
         check(lib().tx_kv_cache_export(self.handle, req_id, part, layer, VP(out.data_ptr()), VP(_stream(stream))))
         return out

@@ -52,6 +52,33 @@ def test_counts_and_sizes(L):
     assert L.tx_kv_pool_bytes(ctypes.byref(c), 10, 4, 1000) >= 10 * L.tx_kv_page_bytes(ctypes.byref(c)) + 4 * 16 * 4
 
 
+def test_sparse_config_counts_and_errors(L):
+    """Local-global sparse cross-attention: one more weight tensor (the pooling
+    vector) and per-request global-token records in the pool; invalid or
+    unsupported windows are rejected."""
+    base = _cfg()
+    for kw in (dict(l_local=10, global_pool=True), dict(l_local=10, global_pool=False)):
+        m = I.ModelConfig(**{**I.workload("headline").model.__dict__, **kw})
+        c = T.Config.of(m)
+        assert L.tx_num_weights(ctypes.byref(c)) == I.n_weights(m)
+    c = _cfg(l_local=10, global_pool=True)
+    d, n_dec, req = 1024, 2, 4
+    extra = L.tx_kv_pool_bytes(ctypes.byref(c), 10, req, 1000) - L.tx_kv_pool_bytes(ctypes.byref(base), 10, req, 1000)
+    assert extra >= req * (2 * 4 + d * 4 + 2 * n_dec * d * 2)
+    assert L.tx_kv_pool_bytes(ctypes.byref(_cfg(l_local=10)), 10, req, 1000) == \
+        L.tx_kv_pool_bytes(ctypes.byref(base), 10, req, 1000)
+    h = T.VP()
+    for kw, code in ((dict(l_local=-1), T.TX_E_INVALID), (dict(l_local=65), T.TX_E_UNSUPPORTED),
+                     (dict(l_local=0, global_pool=True), T.TX_E_INVALID)):
+        bad = _cfg(**kw)
+        assert L.tx_model_create(ctypes.byref(bad), T.VP(FAKE_REPACK), 1 << 30, 1, ctypes.byref(h)) == code, kw
+    bad = _cfg(l_local=4)
+    bad.global_pool = 2
+    assert L.tx_model_create(ctypes.byref(bad), T.VP(FAKE_REPACK), 1 << 30, 1, ctypes.byref(h)) == T.TX_E_INVALID
+    m = _model(L, _cfg(l_local=64, global_pool=True))
+    L.tx_model_destroy(m)
+
+
 def _model(L, cfg):
     h = T.VP()
     rc = L.tx_model_create(ctypes.byref(cfg), T.VP(FAKE_REPACK), L.tx_model_repack_bytes(ctypes.byref(cfg)), 7,

@@ -1,0 +1,135 @@
+"""Parity of the local-global sparse cross-attention (HIP path through the C
+ABI) with the fp64 oracle (Sec. 4.1.2: each decoder query attends to the last
+L_local cached tokens plus an attention-pooled global token).
+
+Cases cover windows longer than the history, windows ending exactly on a page
+boundary and windows straddling two pages, the pooled token built in one pass,
+folded in over appended events, and exported directly; with and without the
+pooled token; fp32 and bf16, d_head 64 and 128.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from paper_2607_28940_amd import inputs as I
+from paper_2607_28940_amd.inputs import ModelConfig
+from tests.parity_util import BF16_TOL, FP32_TOL, DeviceCase, log, oracle_request, score_err, tensor_err
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    torch.cuda.set_device(0)
+
+
+def _sparse(model, l_local=10, pool=True):
+    return dataclasses.replace(model, l_local=l_local, global_pool=pool)
+
+
+def _compare(run, orc, reqs, tol, label, append=False):
+    g = np.concatenate(run.score(reqs))
+    o = np.concatenate([oracle_request(orc, run.wl, r, append=append)[0] for r in reqs])
+    err = score_err(g, o)
+    log(f"{label}: max err {err['max']:.3e} p99 {err['p99']:.3e} (tol {tol})")
+    assert np.all(np.isfinite(g))
+    assert err["max"] <= tol, err
+    return g, o
+
+
+def test_tiny_fp32_sparse(oracle_mod):
+    wl0 = I.workload("tiny")
+    m = _sparse(wl0.model, l_local=10)
+    wl = dataclasses.replace(wl0, model=m)
+    w = I.make_weights(m, ("sharp", "affine"))
+    log("tiny fp32 sparse")
+    run = DeviceCase(wl, w)
+    run.build([0])
+    _compare(run, oracle_mod.Oracle(m, w), [0], FP32_TOL, "tiny fp32 sparse")
+
+
+# histories: window longer than the history (1, 6), exactly the window (10),
+# a window ending on a page boundary (64, 128) and one straddling two pages (70)
+RAGGED = dict(L=[70, 1, 128, 10, 6, 64, 200], S=[5, 3, 0, 70, 2, 4, 9], C=[7, 1, 40, 33, 5, 64, 100])
+SHARP = ("sharp", "affine")
+# The window and page indexing is pinned at the fp32 bar with sharp attention
+# (logits of a few units: a misplaced key moves the scores far beyond 1e-4).
+# In bf16 the same sharp logits make the rounding of Q and K alone move the
+# softmax weights by percents; with few keys per query there is little
+# averaging, and a 64-token window reaches 2.3e-2 on one request of this
+# workload (the dense path 1.6e-2), so the bf16 64-token case uses the
+# standard attention weights and keeps the 2e-2 bar.
+CASES = [
+    ("f32-dh64-L64-pool", ModelConfig(128, 2, 256, 1, 2, rel_pos_buckets=16, dtype="f32"), 64, True, SHARP,
+     FP32_TOL),
+    ("f32-dh32-L10-pool", ModelConfig(64, 2, 256, 1, 2, rel_pos_buckets=8, dtype="f32"), 10, True, SHARP, FP32_TOL),
+    ("dh128-L10-pool", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16), 10, True, SHARP, BF16_TOL),
+    ("dh64-L10-pool", ModelConfig(256, 4, 512, 2, 2, rel_pos_buckets=16), 10, True, SHARP, BF16_TOL),
+    ("dh128-L64-pool", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16), 64, True, ("affine",), BF16_TOL),
+    ("dh64-L5-nopool", ModelConfig(256, 4, 512, 2, 1, rel_pos_buckets=0), 5, False, SHARP, BF16_TOL),
+]
+
+
+@pytest.mark.parametrize("name,model,l_local,pool,variant,tol", CASES, ids=[c[0] for c in CASES])
+def test_sparse_ragged(oracle_mod, name, model, l_local, pool, variant, tol):
+    m = _sparse(model, l_local, pool)
+    wl = I.custom_workload(m, cfg_id=41, **RAGGED)
+    w = I.make_weights(m, variant)
+    log(f"sparse {name}")
+    run = DeviceCase(wl, w)
+    run.build(range(wl.B))
+    _compare(run, oracle_mod.Oracle(m, w), range(wl.B), tol, f"sparse {name}")
+
+
+def test_global_token_export_vs_oracle(oracle_mod):
+    m = _sparse(ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16))
+    wl = I.custom_workload(m, cfg_id=42, L=[150, 3], S=[2, 2], C=[3, 3])
+    w = I.make_weights(m, ("sharp", "affine"))
+    run = DeviceCase(wl, w)
+    run.build([0, 1])
+    orc = oracle_mod.Oracle(m, w)
+    for r in (0, 1):
+        _, st = oracle_request(orc, wl, r)
+        Kg, Vg = orc.cross_kv(orc.pool(st["H"])[None, :])
+        for part, ref in ((4, Kg), (5, Vg)):
+            for layer in range(m.n_dec_layers):
+                g = run.cache.export(r, part, layer).float().cpu().numpy()
+                e = tensor_err(g, ref[layer])
+                log(f"global token r{r} part{part} layer{layer}: {e:.3e}")
+                assert e < 5e-2, (r, part, layer, e)
+
+
+def test_sparse_append_folds_pooling_state(oracle_mod):
+    """Appending events folds only the new rows into the stored pooling state;
+    the result matches pooling the rebuilt history (App. D: incremental
+    encoding) and the oracle's scores after the append."""
+    m = _sparse(ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16))
+    wl = I.custom_workload(m, cfg_id=43, L=[60, 130, 5], S=[6, 2, 3], C=[9, 17, 4], n_append=13)
+    w = I.make_weights(m, ("sharp", "affine"))
+    inc = DeviceCase(wl, w)
+    inc.build([0, 1, 2])
+    inc.append([0, 1, 2], 0, 5)   # 60 -> 65 crosses a page boundary
+    inc.append([0, 1, 2], 5, 13)  # 5 -> 18: the window now lies inside the appended events
+    full = DeviceCase(wl, w)
+    X = [np.concatenate([I.request_tokens(wl, r, I.STREAM_BEHAVIOR), I.request_tokens(wl, r, I.STREAM_EVENTS)])
+         for r in (0, 1, 2)]
+    full.cache.build([0, 1, 2], full.dev(np.concatenate(X)), I.offsets([len(x) for x in X]))
+    for r in (0, 1, 2):
+        for part in (4, 5):
+            for layer in range(m.n_dec_layers):
+                a = inc.cache.export(r, part, layer).float().cpu().numpy()
+                b = full.cache.export(r, part, layer).float().cpu().numpy()
+                e = tensor_err(a, b)
+                log(f"global token append vs rebuild r{r} part{part} layer{layer}: {e:.3e}")
+                assert e < 2e-2
+    g_inc = np.concatenate(inc.score([0, 1, 2]))
+    g_full = np.concatenate(full.score([0, 1, 2]))
+    assert score_err(g_inc, g_full)["max"] < 1e-2
+    orc = oracle_mod.Oracle(m, w)
+    o = np.concatenate([oracle_request(orc, wl, r, append=True)[0] for r in (0, 1, 2)])
+    err = score_err(g_inc, o)
+    log(f"sparse append scores vs oracle: {err}")
+    assert err["max"] <= BF16_TOL
