@@ -8,6 +8,8 @@ head. The caches are built (untimed) before the timed region; inputs are
 resident in HBM when it starts. Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload headline]
+  python bench.py --l-local 10        # local-global sparse cross-attention
+                                      # (last 10 cached tokens + pooled token)
 
 The JSON carries the roofline of the dominant kernel, whose per-launch time
 comes from HIP events the library records around each launch on the stream
@@ -16,6 +18,7 @@ comes from HIP events the library records around each launch on the stream
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import math
 import os
@@ -30,6 +33,14 @@ PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 METRIC = "candidate scores/sec + % bf16 MFMA peak, B=256 L=4096 C=512 on 1 MI355X"
+
+
+def cross_keys(m, L: int) -> int:
+    """Keys each decoder query attends to: the whole cache, or the
+    local-global sparse set (last l_local tokens, plus the pooled token)."""
+    if m.l_local <= 0:
+        return L
+    return min(L, m.l_local) + (1 if m.global_pool else 0)
 
 
 def score_work(wl):
@@ -48,10 +59,10 @@ def score_work(wl):
             last = layer == m.n_dec_layers - 1
             rows = C if last else N
             f_gemm += (12 * d * d + 4 * d * F) * rows + (4 * d * d * S if last else 0)
-            f_cross += 4.0 * L * d * rows
+            f_cross += 4.0 * cross_keys(m, L) * d * rows
             f_self += (0 if last else 2.0 * d * S * (S + 1)) + 4.0 * d * C * (S + 1)
         f_gemm += 2 * d * C
-    kv = sum(m.n_dec_layers * 2 * L * d for L in wl.L) * es
+    kv = sum(m.n_dec_layers * 2 * cross_keys(m, L) * d for L in wl.L) * es
     tok = sum(S + C for S, C in zip(wl.S, wl.C)) * d * es
     wts = m.n_dec_layers * (12 * d * d + 2 * d * F) * es
     return {"flop": f_gemm + f_cross + f_self, "flop_gemm": f_gemm, "flop_cross": f_cross, "flop_self": f_self,
@@ -72,8 +83,9 @@ def cpu_baseline(wl, weights, n_req: int):
     elapsed = 0.0
     for r in range(n_req):
         rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([I.SEED_X, wl.cfg_id, 7, r])))
-        Kx = rng.standard_normal((m.n_dec_layers, wl.L[r], m.d_model))
-        Vx = rng.standard_normal((m.n_dec_layers, wl.L[r], m.d_model))
+        nk = cross_keys(m, wl.L[r])
+        Kx = rng.standard_normal((m.n_dec_layers, nk, m.d_model))
+        Vx = rng.standard_normal((m.n_dec_layers, nk, m.d_model))
         Xs = I.request_tokens(wl, r, I.STREAM_SERVING)
         Xc = I.request_tokens(wl, r, I.STREAM_CANDIDATES)
         t0 = time.perf_counter()
@@ -118,7 +130,12 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="headline", choices=["headline", "uniform", "ragged", "tiny"])
-    ap.add_argument("--cpu-requests", type=int, default=4)
+    ap.add_argument("--l-local", type=int, default=0,
+                    help="local-global sparse cross-attention window (0: dense cross-attention, the headline)")
+    ap.add_argument("--no-global-token", action="store_true",
+                    help="with --l-local: no attention-pooled global token")
+    ap.add_argument("--cpu-requests", type=int, default=None,
+                    help="requests in the oracle's timed sample (default: about 10 s of CPU work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-launch events")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
@@ -140,6 +157,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a ROCm GPU"
     torch.cuda.set_device(0)
     wl = I.workload(args.workload)
+    if args.l_local > 0:
+        wl = dataclasses.replace(wl, model=dataclasses.replace(wl.model, l_local=args.l_local,
+                                                               global_pool=not args.no_global_token))
     m = wl.model
     t_setup = time.time()
     weights = I.make_weights(m)
@@ -221,10 +241,19 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, weights, min(args.cpu_requests, wl.B))
+        n_cpu = args.cpu_requests or (32 if m.l_local > 0 else 4)
+        cpu = cpu_baseline(wl, weights, min(n_cpu, wl.B))
 
+    sparse = m.l_local > 0
+    if sparse:
+        mode = f"local-global sparse cross-attention (last {m.l_local} cached tokens" + \
+               (" + pooled global token)" if m.global_pool else ")")
+        metric = f"candidate scores/sec, {args.workload} with {mode} on 1 MI355X"
+    else:
+        mode = "dense cross-attention over every cached token"
+        metric = METRIC if args.workload == "headline" else f"candidate scores/sec, {args.workload} on 1 MI355X"
     line = {
-        "metric": METRIC if args.workload == "headline" else f"candidate scores/sec, {args.workload} on 1 MI355X",
+        "metric": metric,
         "value": round(value, 1), "unit": "scores/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": m.dtype, "data": "synthetic (seeded N(0,1) tokens, N(0,0.02) weights)",
@@ -232,7 +261,7 @@ def main():
                                f"S={'ragged' if len(set(wl.S)) > 1 else wl.S[0]} "
                                f"C={'ragged' if len(set(wl.C)) > 1 else wl.C[0]} d={m.d_model} H={m.n_heads} "
                                f"F={m.d_ffn} n_enc={m.n_enc_layers} n_dec={m.n_dec_layers} page=64",
-                   "global_batch": wl.B, "scores_per_step": n_scores},
+                   "global_batch": wl.B, "scores_per_step": n_scores, "cross_attention": mode},
         "mfma_frac_of_peak": round(tflops / peak, 4),
         "achieved_tflops": round(tflops, 2),
         "algorithmic": {"flop_per_step": work["flop"], "bytes_per_step": work["bytes"]},

@@ -119,10 +119,16 @@ hipError_t launch_store_rows(bool bf, const void* src, int W, const PoolReq* req
 
 // ---------------------------------------------------------------- attention
 
-// One block per tile of 64 queries of one (request, head): the at most 65 keys
-// and values go to LDS as fp32 (V read back from the page's transposed,
-// k-permuted layout), then every query is served by 4 lanes, each owning
-// DH/4 features, with the online softmax in the exp2 domain.
+// One block per tile of 64 queries of one (request, head): the keys and
+// values (at most l_local + 1) go to LDS as fp32, sized for the launch's
+// window so that many blocks share a CU (K rows are read feature-fastest, V
+// from the page's transposed, k-permuted layout key-fastest, both
+// contiguous), then every query is served by 4 lanes, each owning DH/4
+// features, with the online softmax in the exp2 domain. In LDS each key row
+// keeps the four lanes' feature runs 16-byte aligned and DH/4 + 4 floats
+// apart, so a lane reads its run with 16-byte loads and the four runs of a
+// query fall in different banks (the 16 queries of a wave read the same row:
+// broadcast).
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void lg_cross_attn(const T* __restrict__ q, int ldq, T* __restrict__ out, int ldo,
                                                      const T* __restrict__ pool, const int32_t* __restrict__ page_table,
@@ -131,9 +137,11 @@ __global__ __launch_bounds__(256) void lg_cross_attn(const T* __restrict__ q, in
                                                      const AttnTile* __restrict__ tiles, int l_local,
                                                      const T* __restrict__ gkv, int gkv_ld, int dec_layer,
                                                      float scale_log2) {
-  constexpr int DP = DH / 4;
-  __shared__ float sK[kMaxLocal + 1][DH + 1];
-  __shared__ float sV[kMaxLocal + 1][DH + 1];
+  constexpr int DP = DH / 4, PS = DP + 4, LD = 4 * PS;  // part stride, row stride (floats)
+  extern __shared__ __attribute__((aligned(16))) float smem[];
+  float* sK = smem;                               // [l_local + 1][LD]
+  float* sV = smem + (size_t)(l_local + 1) * LD;  // [l_local + 1][LD]
+  auto at = [](int j, int f) { return j * LD + (f / DP) * PS + (f % DP); };
   const AttnTile tile = tiles[blockIdx.x];
   if (tile.q_count <= 0) return;
   const AttnReq rq = reqs[tile.req];
@@ -142,19 +150,24 @@ __global__ __launch_bounds__(256) void lg_cross_attn(const T* __restrict__ q, in
   const int k0 = max(0, len - l_local), nl = len - k0;
   const int32_t* ptab = page_table + (size_t)rq.slot * max_pages;
   for (int e = tid; e < nl * DH; e += 256) {
-    const int j = e / DH, f = e % DH;
-    const int pos = k0 + j, t = pos % kPage;
+    const int j = e / DH, f = e % DH;  // feature fastest: one K row is contiguous
+    const int pos = k0 + j;
     const T* base = pool + (size_t)ptab[pos / kPage] * g.page_elems;
-    sK[j][f] = (float)base[g.k_off(layer_slot, h) + (size_t)t * DH + f];
-    sV[j][f] = (float)base[g.v_off(layer_slot, h) + (size_t)f * kPage + vt_col(t)];
+    sK[at(j, f)] = (float)base[g.k_off(layer_slot, h) + (size_t)(pos % kPage) * DH + f];
+  }
+  for (int e = tid; e < nl * DH; e += 256) {
+    const int f = e / nl, j = e % nl;  // key fastest: one V^T row is contiguous
+    const int pos = k0 + j;
+    const T* base = pool + (size_t)ptab[pos / kPage] * g.page_elems;
+    sV[at(j, f)] = (float)base[g.v_off(layer_slot, h) + (size_t)f * kPage + vt_col(pos % kPage)];
   }
   int nk = nl;
   if (gkv) {
     const int d = g.H * DH;
     const T* kr = gkv + (size_t)rq.slot * gkv_ld + (size_t)(2 * dec_layer) * d + h * DH;
     for (int f = tid; f < DH; f += 256) {
-      sK[nl][f] = (float)kr[f];
-      sV[nl][f] = (float)kr[d + f];
+      sK[at(nl, f)] = (float)kr[f];
+      sV[at(nl, f)] = (float)kr[d + f];
     }
     ++nk;
   }
@@ -170,18 +183,28 @@ __global__ __launch_bounds__(256) void lg_cross_attn(const T* __restrict__ q, in
   }
   float m = -INFINITY, l = 0.f;
   for (int j = 0; j < nk; ++j) {
+    const floatx4* kr = reinterpret_cast<const floatx4*>(sK + j * LD + part * PS);
+    const floatx4* vr = reinterpret_cast<const floatx4*>(sV + j * LD + part * PS);
     float s = 0.f;
 #pragma unroll
-    for (int e = 0; e < DP; ++e) s = fmaf(qv[e], sK[j][part * DP + e], s);
+    for (int e = 0; e < DP / 4; ++e) {
+      const floatx4 k4 = kr[e];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) s = fmaf(qv[4 * e + c], k4[c], s);
+    }
     s += __shfl_xor(s, 1);
     s += __shfl_xor(s, 2);
     s *= scale_log2;
     const float m_new = fmaxf(m, s);
-    const float alpha = exp2f(m - m_new);
-    const float p = exp2f(s - m_new);
+    const float alpha = __builtin_amdgcn_exp2f(m - m_new);  // 0 while m is -inf
+    const float p = __builtin_amdgcn_exp2f(s - m_new);
     l = l * alpha + p;
 #pragma unroll
-    for (int e = 0; e < DP; ++e) acc[e] = fmaf(p, sV[j][part * DP + e], acc[e] * alpha);
+    for (int e = 0; e < DP / 4; ++e) {
+      const floatx4 v4 = vr[e];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[4 * e + c] = fmaf(p, v4[c], acc[4 * e + c] * alpha);
+    }
     m = m_new;
   }
   const float inv = 1.f / l;
@@ -196,8 +219,9 @@ hipError_t launch_lg_attention(bool bf, const void* q, int ldq, void* out, int l
   if (n_tiles <= 0) return hipSuccess;
   if (l_local < 1 || l_local > kMaxLocal) return hipErrorInvalidValue;
   const float sl2 = 1.4426950408889634f / sqrtf((float)g.dh);
-#define TX_LG(TT, DH)                                                                                          \
-  lg_cross_attn<TT, DH><<<n_tiles, 256, 0, s>>>((const TT*)q, ldq, (TT*)out, ldo, (const TT*)pool, page_table, \
+  const size_t lds = (size_t)(l_local + 1) * 4 * (g.dh / 4 + 4) * 2 * sizeof(float);
+#define TX_LG(TT, DH)                                                                                            \
+  lg_cross_attn<TT, DH><<<n_tiles, 256, lds, s>>>((const TT*)q, ldq, (TT*)out, ldo, (const TT*)pool, page_table, \
                                                 max_pages, g, layer_slot, reqs, tiles, l_local, (const TT*)gkv,  \
                                                 gkv_ld, dec_layer, sl2)
   switch (g.dh) {

@@ -65,6 +65,24 @@ def test_headline_full(oracle_mod):
     torch.cuda.empty_cache()
 
 
+def test_headline_sparse_full(oracle_mod):
+    """The headline batch with the local-global sparse cross-attention the
+    paper's experiments use (Sec. 5 setup: last 10 cached tokens plus an
+    attention-pooled global token), in the launch configuration
+    bench.py --l-local 10 times; the oracle recomputes one sampled request."""
+    import dataclasses
+    import torch
+    wl0 = I.workload("headline")
+    m = dataclasses.replace(wl0.model, l_local=10, global_pool=True)
+    wl = dataclasses.replace(wl0, model=m)
+    w = I.make_weights(m)
+    log("headline sparse: building 256 caches")
+    run = DeviceCase(wl, w)
+    _build_all(run, 128)
+    _check_sampled(run, oracle_mod.Oracle(m, w), [77], "headline sparse")
+    torch.cuda.empty_cache()
+
+
 @pytest.fixture(autouse=True)
 def _free_memory():
     yield
