@@ -57,7 +57,8 @@ def _load(path: Optional[str] = None):
         lib.ox_cross_kv.argtypes = [P(_Cfg), wp, dp, ctypes.c_int, dp, dp]
         lib.ox_score.argtypes = [P(_Cfg), wp, dp, dp, ctypes.c_int, dp, ctypes.c_int, dp, ctypes.c_int, dp, dp, dp]
         lib.ox_pool.argtypes = [ctypes.c_int, dp, ctypes.c_int, dp, dp]
-        for f in ("ox_encode", "ox_encode_append", "ox_cross_kv", "ox_score", "ox_pool"):
+        lib.ox_actions.argtypes = [ctypes.c_int, ctypes.c_int, dp, ctypes.c_int, dp, dp, dp]
+        for f in ("ox_encode", "ox_encode_append", "ox_cross_kv", "ox_score", "ox_pool", "ox_actions"):
             getattr(lib, f).restype = None
         _libs[path] = lib
     return _libs[path]
@@ -132,18 +133,37 @@ class Oracle:
         self.lib.ox_cross_kv(ctypes.byref(self.cfg), self._wp, _dp(Henc), L, _dp(K), _dp(V))
         return K, V
 
+    @property
+    def n_actions(self) -> int:
+        return int(getattr(self.model, "n_actions", 0))
+
+    def actions(self, Z) -> np.ndarray:
+        """Query-key softmax over the model's k action tokens for decoder
+        outputs Z [C, d] -> probabilities [C, k]."""
+        Z = _f64(Z)
+        k = self.n_actions
+        n = len(self._w)
+        W, b = self._w[n - 2], self._w[n - 1]
+        P = np.empty((Z.shape[0], k))
+        self.lib.ox_actions(self.d, k, _dp(Z), Z.shape[0], _dp(W), _dp(b), _dp(P))
+        return P
+
     def score(self, Kx, Vx, Xs, Xc, trace: bool = False):
-        """Decoder + head. Returns scores [C] (and, with trace=True, also the
-        per-layer sublayer outputs [n_dec, 3, S+C, d] and the max softmax
-        row-sum deviation)."""
+        """Decoder + head. Returns scores [C] (the candidate logit) or, for a
+        model with k action tokens, probabilities [C, k]; with trace=True also
+        the per-layer sublayer outputs [n_dec, 3, S+C, d] and the max softmax
+        row-sum deviation."""
         Kx, Vx, Xs, Xc = _f64(Kx), _f64(Vx), _f64(Xs), _f64(Xc)
         L = Kx.shape[1]
         S, C = Xs.shape[0], Xc.shape[0]
         out = np.empty(C)
-        tr = np.empty((self.model.n_dec_layers, 3, S + C, self.d)) if trace else None
+        want_z = self.n_actions > 0
+        tr = np.empty((self.model.n_dec_layers, 3, S + C, self.d)) if (trace or want_z) else None
         err = np.zeros(1)
         self.lib.ox_score(ctypes.byref(self.cfg), self._wp, _dp(Kx), _dp(Vx), L, _dp(Xs), S, _dp(Xc), C, _dp(out),
                           _dp(tr), _dp(err))
+        if want_z:  # the scalar head output is meaningless here: apply the action decoder
+            out = self.actions(tr[-1, 2, S:])
         if trace:
             return out, tr, float(err[0])
         return out

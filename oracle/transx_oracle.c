@@ -19,7 +19,8 @@
  *     (Sec. 4.1.2, Eq. sparse-cross-attn with the index set = all tokens),
  *     the crossAttend residual/LayerNorm block (Sec. 4.1.2) and an FFN,
  *   - a linear scalar head on the candidate rows (the k = 2 case of Sec. 4.1.3,
- *     Eq. action-decoding),
+ *     Eq. action-decoding), or the query-key softmax over k action tokens
+ *     itself (ox_actions),
  *   - incremental append: only the new tokens are encoded, against the stored
  *     per-layer keys/values of the prefix (App. D, remark on incremental
  *     encoding; Sec. 4.2, causal attention and prefix reuse),
@@ -377,4 +378,29 @@ void ox_pool(int d, const double* Henc, int L, const double* w, double* g) {
     for (int k = 0; k < d; ++k) g[k] += a * Henc[(size_t)j * d + k];
   }
   free(z);
+}
+
+/*
+ * Query-key softmax decoder over k action tokens (Sec. 4.1.3, Eq.
+ * action-decoding): for each candidate c with decoder output z_c (the key
+ * k_dec = f_dec(z_c); here f_dec is the decoder stack itself, the
+ * Transformer-based head of App. B), P[c][a] = softmax over a of
+ * (z_c . W[:, a] + b[a]), with the action embeddings as the columns of W
+ * [d][k] and a per-action offset b [k].
+ */
+void ox_actions(int d, int k, const double* Z, int C, const double* W, const double* b, double* P) {
+  double* logit = (double*)malloc(sizeof(double) * (size_t)(k > 0 ? k : 1));
+  for (int c = 0; c < C; ++c) {
+    double mx = -INFINITY;
+    for (int a = 0; a < k; ++a) {
+      double s = b[a];
+      for (int i = 0; i < d; ++i) s += Z[(size_t)c * d + i] * W[(size_t)i * k + a];
+      logit[a] = s;
+      if (s > mx) mx = s;
+    }
+    double den = 0.0;
+    for (int a = 0; a < k; ++a) den += exp(logit[a] - mx);
+    for (int a = 0; a < k; ++a) P[(size_t)c * k + a] = exp(logit[a] - mx) / den;
+  }
+  free(logit);
 }

@@ -52,6 +52,10 @@ class ModelConfig:
     # when global_pool is set
     l_local: int = 0
     global_pool: bool = False
+    # decoder head (Sec. 4.1.3): 0 = one logit per candidate (the two-action
+    # case, linear head w_s, b_s); k >= 2 = softmax over k learned action
+    # embeddings (W_dec [d, k], b_dec [k]), k probabilities per candidate
+    n_actions: int = 0
 
     @property
     def d_head(self) -> int:
@@ -104,8 +108,12 @@ def weight_specs(m: ModelConfig) -> List[tuple]:
             if shp is None:
                 shp = (d, d) if n.endswith(("Wq", "Wk", "Wv", "Wo")) else (d,)
             out.append(("dec", l, n, shp))
-    out.append(("head", 0, "w_s", (d,)))
-    out.append(("head", 0, "b_s", (1,)))
+    if m.n_actions:
+        out.append(("head", 0, "W_dec", (d, m.n_actions)))
+        out.append(("head", 0, "b_dec", (m.n_actions,)))
+    else:
+        out.append(("head", 0, "w_s", (d,)))
+        out.append(("head", 0, "b_s", (1,)))
     if m.global_pool:
         out.append(("pool", 0, "w_pool", (d,)))
     return out
@@ -141,7 +149,9 @@ def make_weights(m: ModelConfig, variant: Sequence[str] = (), seed_w: int = SEED
       units and softmax is far from uniform.
     variant "affine": LayerNorm gain 1 + N(0, 0.1), offset N(0, 0.1).
     The pooling vector of the global token is N(0, 0.02) (nearly uniform
-    pooling), N(0, 16) under "sharp" (pooling logits of a few units).
+    pooling), N(0, 16) under "sharp" (pooling logits of a few units); the
+    action embeddings W_dec are N(0, (4/sqrt d)^2) under "sharp" (action
+    logits of a few units).
     """
     variant = set(variant)
     d = m.d_model
@@ -157,6 +167,8 @@ def make_weights(m: ModelConfig, variant: Sequence[str] = (), seed_w: int = SEED
             w = (1.0 if "sharp" in variant else 0.02) * z
         elif name == "w_pool":
             w = (4.0 if "sharp" in variant else 0.02) * z
+        elif name == "W_dec" and "sharp" in variant:
+            w = (4.0 / math.sqrt(d)) * z
         elif "sharp" in variant and name in ("Wq", "Wk", "sWq", "sWk", "xWq", "xWk"):
             w = (2.0 / math.sqrt(d)) * z
         else:

@@ -83,8 +83,12 @@ class TorchTransX:
                     ln.weight.copy_(_t(p[f"ln{k}_g"]))
                     ln.bias.copy_(_t(p[f"ln{k}_b"]))
                 self.dec_layers.append(layer)
-        self.w_s = _t(head[0]).reshape(-1)
-        self.b_s = float(np.asarray(head[1]).reshape(-1)[0])
+        if m.n_actions:
+            self.W_dec = _t(head[0]).reshape(d, m.n_actions)
+            self.b_dec = _t(head[1]).reshape(-1)
+        else:
+            self.w_s = _t(head[0]).reshape(-1)
+            self.b_s = float(np.asarray(head[1]).reshape(-1)[0])
 
     def _enc_mask(self, e: int, L: int) -> torch.Tensor:
         H, R = self.m.n_heads, self.m.rel_pos_buckets
@@ -129,6 +133,8 @@ class TorchTransX:
             for layer in self.dec_layers:
                 t = layer(t, mem, tgt_mask=mask)
         z = t[0, S:].detach()
+        if self.m.n_actions:
+            return torch.softmax(z @ self.W_dec + self.b_dec, dim=-1).numpy()
         return (z @ self.w_s + self.b_s).numpy()
 
     def memory(self, Henc) -> torch.Tensor:
