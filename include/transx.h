@@ -75,6 +75,12 @@ typedef struct {
    * layer's cross-attention K/V weights. global_pool requires l_local > 0. */
   int32_t l_local;
   int32_t global_pool;
+  /* Decoder head (Sec. 4.1.3, Eq. action-decoding). 0: one logit per
+   * candidate, s = z . w_s + b_s (the two-action case). k = 2..16: the
+   * query-key softmax over k learned action embeddings, p = softmax(z W_dec +
+   * b_dec), W_dec [d_model][k] (column a = action a's embedding), where z is
+   * the candidate's decoder output row. */
+  int32_t n_actions;
 } tx_config;
 
 typedef struct tx_model tx_model;
@@ -90,7 +96,7 @@ const char* tx_last_error(void);
  *   per decoder layer (26): self Wq bq Wk bk Wv bv Wo bo ln1_g ln1_b,
  *                           cross Wq bq Wk bk Wv bv Wo bo ln2_g ln2_b,
  *                           FFN W1 b1 W2 b2 ln3_g ln3_b
- *   head (2): w_s[d] b_s[1]
+ *   head (2): w_s[d] b_s[1], or with n_actions = k: W_dec[d][k] b_dec[k]
  *   global-token pooling (1, only when global_pool): w_pool[d]
  * Matrices are [d_in][d_out] row-major (a layer computes y = x W + b). */
 int32_t tx_num_weights(const tx_config* cfg);
@@ -215,7 +221,9 @@ int kv_cache_append(tx_kv_cache* cache, int32_t n_req, const int32_t* req_ids /*
  *                      token of its request and itself, never another candidate
  *   candidate_offsets  host [n_req+1], C_i >= 0
  *   scores             device fp32 [sum C]: scores[candidate_offsets[i] + c] is the
- *                      logit of candidate c of request i (sigmoid = click probability)
+ *                      logit of candidate c of request i (sigmoid = click probability);
+ *                      with n_actions = k, [sum C][k]: row candidate_offsets[i] + c holds
+ *                      that candidate's probabilities over the k actions (sum 1)
  * A request with C_i = 0 contributes nothing. Errors: TX_E_NOCACHE (a request
  * has no cache: cold start, App. D), TX_E_INVALID, TX_E_NOMEM, TX_E_HIP. */
 int score_candidates(const tx_kv_cache* cache, int32_t n_req, const int32_t* req_ids /* host */,

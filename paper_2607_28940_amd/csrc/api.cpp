@@ -97,6 +97,7 @@ struct tx_model {
   float* wpool = nullptr;  // attention-pooling vector of the global token [d]
   int l_local = 0;         // > 0: local-global sparse cross-attention
   bool gpool = false;      // the sparse key set includes the pooled global token
+  int n_act = 0;           // 0: scalar logit head (ws [d], bs [1]); k: ws [d][k], bs [k]
   bool weights_set = false;
 };
 
@@ -117,6 +118,8 @@ static int check_config(const tx_config* c) {
   if (c->global_pool != 0 && c->global_pool != 1) return fail(TX_E_INVALID, "global_pool %d", c->global_pool);
   if (c->global_pool && c->l_local == 0)
     return fail(TX_E_INVALID, "the pooled global token belongs to the sparse cross-attention (l_local > 0)");
+  if (c->n_actions < 0 || c->n_actions == 1) return fail(TX_E_INVALID, "n_actions %d (0 or >= 2)", c->n_actions);
+  if (c->n_actions > kMaxActions) return fail(TX_E_UNSUPPORTED, "n_actions %d above %d", c->n_actions, kMaxActions);
   return TX_OK;
 }
 
@@ -152,8 +155,9 @@ static void layout_model(const tx_config& c, Carver& cv, tx_model& m) {
     L.ln1g = vec(d), L.ln1b = vec(d), L.ln2g = vec(d), L.ln2b = vec(d), L.ln3g = vec(d), L.ln3b = vec(d);
   }
   m.xkv = mat(2 * d * c.n_dec_layers, d);
-  m.ws = vec(d);
-  m.bs = vec(1);
+  const int k = std::max(1, c.n_actions);
+  m.ws = vec((size_t)d * k);
+  m.bs = vec(k);
   if (c.global_pool) m.wpool = vec(d);
 }
 
@@ -195,6 +199,7 @@ int tx_model_create(const tx_config* cfg, void* dev_repack, size_t repack_bytes,
   m->esz = m->bf ? 2 : 4;
   m->l_local = cfg->l_local;
   m->gpool = cfg->global_pool != 0;
+  m->n_act = cfg->n_actions;
   Carver cv(dev_repack);
   layout_model(*cfg, cv, *m);
   *out = m;
@@ -273,8 +278,9 @@ int tx_model_set_weights(tx_model* m, const void* const* W, int32_t n_weights, h
     run(bias(b + D_LN3B, L.ln3b, d));
   }
   const int hb = E_N * m->n_enc + D_N * m->n_dec;
-  run(bias(hb, m->ws, d));
-  run(bias(hb + 1, m->bs, 1));
+  const int k = std::max(1, m->n_act);
+  run(bias(hb, m->ws, (int64_t)d * k));  // [d] or [d][k], kept in that order
+  run(bias(hb + 1, m->bs, k));
   if (m->gpool) run(bias(hb + 2, m->wpool, d));
   if (e != hipSuccess) return fail(TX_E_HIP, "weight repack launch failed: %s", hipGetErrorString(e));
   m->weights_set = true;
@@ -1124,9 +1130,12 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, int a, int b, const
     TX_LAUNCH(K_GEMM_FFN2, f2.first, f2.second,
               launch_gemm(bf, Hf + (size_t)r0 * F * es, F, L.f2.w, L.f2.b, T + ro, d, Y + ro, d, Mr, d, F,
                           EPI_BIAS_RESID, st));
-    if (last)
-      TX_LAUNCH(K_LN_SCORE, 2 * Mrd * dd, Mrd * dd * esd + 4 * Mrd,
-                launch_layernorm_score(bf, Y + ro, L.ln3g, L.ln3b, m->ws, m->bs, scores + co[a], Mr, d, eps, st));
+    if (last) {
+      const int k = std::max(1, m->n_act);
+      TX_LAUNCH(K_LN_SCORE, 2 * Mrd * dd * k, Mrd * dd * esd + 4 * Mrd * k,
+                launch_layernorm_score(bf, Y + ro, L.ln3g, L.ln3b, m->ws, m->bs, scores + (size_t)co[a] * k, Mr, d,
+                                       eps, m->n_act, st));
+    }
     else
       TX_LAUNCH(K_LAYERNORM, 0, 2 * Mrd * dd * esd,
                 launch_layernorm(bf, Y + ro, T + ro, L.ln3g, L.ln3b, Mr, d, eps, st));

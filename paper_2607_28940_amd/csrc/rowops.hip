@@ -1,11 +1,51 @@
 // Row-wise and data-movement kernels of the TransX path:
 //   LayerNorm of post-LN sublayers (Sec. 4.1.2 crossAttend block), optionally
-//   fused with the linear scoring head (Sec. 4.1.3, Eq. action-decoding with
-//   two actions reduces to one logit), the scatter of projected K/V rows into
+//   fused with the decoder head (Sec. 4.1.3, Eq. action-decoding: either the
+//   softmax over k action embeddings, or with two actions one logit), the
+//   scatter of projected K/V rows into
 //   the paged cache layout, cache export, and weight repacking.
 #include "tx_internal.h"
 
 namespace tx {
+
+// Decoder head on one wave's row, given this lane's share of the normalised
+// row (z at features f(0..cnt-1), spaced by `stride` from c0). n_act == 0:
+// scores[row] = z . w + b0[0]. n_act = k >= 2: w is [d][k] (action a's
+// embedding in column a), lane a ends up with logit a, and the softmax over
+// the k lanes gives scores[row * k + a].
+template <int CNT>
+__device__ __forceinline__ void head_out(const float (&z)[CNT], int c0, int stride, int cnt, int lane,
+                                         const float* __restrict__ w, const float* __restrict__ b0,
+                                         float* __restrict__ scores, int row, int n_act) {
+  if (n_act == 0) {
+    float dot = 0.f;
+#pragma unroll
+    for (int e = 0; e < CNT; ++e)
+      if (e < cnt) dot += z[e] * w[c0 + e * stride];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) dot += __shfl_xor(dot, o);
+    if (lane == 0) scores[row] = dot + b0[0];
+    return;
+  }
+  float mine = -INFINITY;
+  for (int a = 0; a < n_act; ++a) {
+    float dot = 0.f;
+#pragma unroll
+    for (int e = 0; e < CNT; ++e)
+      if (e < cnt) dot += z[e] * w[(size_t)(c0 + e * stride) * n_act + a];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) dot += __shfl_xor(dot, o);
+    if (lane == a) mine = dot + b0[a];
+  }
+  float mx = mine;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  const float e = lane < n_act ? expf(mine - mx) : 0.f;
+  float den = e;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) den += __shfl_xor(den, o);
+  if (lane < n_act) scores[(size_t)row * n_act + lane] = e / den;
+}
 
 // One wave per row; EPL features per lane held in registers (EPL = d / 64).
 // Two-pass mean / variance in fp32 from the register copy.
@@ -13,7 +53,7 @@ template <typename T, int EPL, bool SCORE>
 __global__ __launch_bounds__(256) void layernorm_rows(const T* __restrict__ x, T* __restrict__ y,
                                                       const float* __restrict__ g, const float* __restrict__ b,
                                                       const float* __restrict__ w, const float* __restrict__ b0,
-                                                      float* __restrict__ scores, int M, int d, float eps) {
+                                                      float* __restrict__ scores, int M, int d, float eps, int n_act) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= M) return;
   const T* xr = x + (size_t)row * d + lane * EPL;
@@ -37,12 +77,10 @@ __global__ __launch_bounds__(256) void layernorm_rows(const T* __restrict__ x, T
   const float inv = rsqrtf(sq / d + eps);
   const int c0 = lane * EPL;
   if (SCORE) {
-    float dot = 0.f;
+    float z[EPL];
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) dot += ((v[e] - mean) * inv * g[c0 + e] + b[c0 + e]) * w[c0 + e];
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) dot += __shfl_xor(dot, o);
-    if (lane == 0) scores[row] = dot + b0[0];
+    for (int e = 0; e < EPL; ++e) z[e] = (v[e] - mean) * inv * g[c0 + e] + b[c0 + e];
+    head_out<EPL>(z, c0, 1, EPL, lane, w, b0, scores, row, n_act);
   } else {
     T* yr = y + (size_t)row * d + c0;
 #pragma unroll
@@ -55,7 +93,8 @@ template <typename T, bool SCORE>
 __global__ __launch_bounds__(256) void layernorm_rows_any(const T* __restrict__ x, T* __restrict__ y,
                                                           const float* __restrict__ g, const float* __restrict__ b,
                                                           const float* __restrict__ w, const float* __restrict__ b0,
-                                                          float* __restrict__ scores, int M, int d, float eps) {
+                                                          float* __restrict__ scores, int M, int d, float eps,
+                                                          int n_act) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= M) return;
   const T* xr = x + (size_t)row * d;
@@ -70,26 +109,30 @@ __global__ __launch_bounds__(256) void layernorm_rows_any(const T* __restrict__ 
   }
   for (int o = 32; o >= 1; o >>= 1) sq += __shfl_xor(sq, o);
   const float inv = rsqrtf(sq / d + eps);
-  float dot = 0.f;
-  for (int c = lane; c < d; c += 64) {
-    const float z = ((float)xr[c] - mean) * inv * g[c] + b[c];
-    if (SCORE) dot += z * w[c];
-    else y[(size_t)row * d + c] = (T)z;
+  if (!SCORE) {
+    for (int c = lane; c < d; c += 64) y[(size_t)row * d + c] = (T)(((float)xr[c] - mean) * inv * g[c] + b[c]);
+    return;
   }
-  if (SCORE) {
-    for (int o = 32; o >= 1; o >>= 1) dot += __shfl_xor(dot, o);
-    if (lane == 0) scores[row] = dot + b0[0];
+  // widths without a register-resident variant are at most 64 * 64 here
+  constexpr int MAXC = 64;
+  float z[MAXC];
+  const int cnt = (d - lane + 63) / 64;
+#pragma unroll
+  for (int e = 0; e < MAXC; ++e) {
+    const int c = lane + 64 * e;
+    z[e] = (e < cnt) ? ((float)xr[c] - mean) * inv * g[c] + b[c] : 0.f;
   }
+  head_out<MAXC>(z, lane, 64, cnt, lane, w, b0, scores, row, n_act);
 }
 
 template <typename T, bool SCORE>
 static hipError_t ln_dispatch(const void* x, void* y, const float* g, const float* b, const float* w, const float* b0,
-                              float* scores, int M, int d, float eps, hipStream_t s) {
+                              float* scores, int M, int d, float eps, int n_act, hipStream_t s) {
   if (M <= 0) return hipSuccess;
   const int blocks = (M + 3) / 4;
   const T* xx = (const T*)x;
   T* yy = (T*)y;
-#define TX_LN(E) layernorm_rows<T, E, SCORE><<<blocks, 256, 0, s>>>(xx, yy, g, b, w, b0, scores, M, d, eps)
+#define TX_LN(E) layernorm_rows<T, E, SCORE><<<blocks, 256, 0, s>>>(xx, yy, g, b, w, b0, scores, M, d, eps, n_act)
   switch (d) {
     case 64: TX_LN(1); break;
     case 128: TX_LN(2); break;
@@ -97,7 +140,9 @@ static hipError_t ln_dispatch(const void* x, void* y, const float* g, const floa
     case 512: TX_LN(8); break;
     case 1024: TX_LN(16); break;
     case 2048: TX_LN(32); break;
-    default: layernorm_rows_any<T, SCORE><<<blocks, 256, 0, s>>>(xx, yy, g, b, w, b0, scores, M, d, eps);
+    default:
+      if (SCORE && d > 64 * 64) return hipErrorInvalidValue;
+      layernorm_rows_any<T, SCORE><<<blocks, 256, 0, s>>>(xx, yy, g, b, w, b0, scores, M, d, eps, n_act);
   }
 #undef TX_LN
   return hipGetLastError();
@@ -105,14 +150,15 @@ static hipError_t ln_dispatch(const void* x, void* y, const float* g, const floa
 
 hipError_t launch_layernorm(bool bf, const void* x, void* y, const float* g, const float* b, int M, int d, float eps,
                             hipStream_t s) {
-  return bf ? ln_dispatch<bf16, false>(x, y, g, b, nullptr, nullptr, nullptr, M, d, eps, s)
-            : ln_dispatch<float, false>(x, y, g, b, nullptr, nullptr, nullptr, M, d, eps, s);
+  return bf ? ln_dispatch<bf16, false>(x, y, g, b, nullptr, nullptr, nullptr, M, d, eps, 0, s)
+            : ln_dispatch<float, false>(x, y, g, b, nullptr, nullptr, nullptr, M, d, eps, 0, s);
 }
 
 hipError_t launch_layernorm_score(bool bf, const void* x, const float* g, const float* b, const float* w,
-                                  const float* b0, float* scores, int M, int d, float eps, hipStream_t s) {
-  return bf ? ln_dispatch<bf16, true>(x, nullptr, g, b, w, b0, scores, M, d, eps, s)
-            : ln_dispatch<float, true>(x, nullptr, g, b, w, b0, scores, M, d, eps, s);
+                                  const float* b0, float* scores, int M, int d, float eps, int n_act, hipStream_t s) {
+  if (n_act < 0 || n_act == 1 || n_act > 64) return hipErrorInvalidValue;
+  return bf ? ln_dispatch<bf16, true>(x, nullptr, g, b, w, b0, scores, M, d, eps, n_act, s)
+            : ln_dispatch<float, true>(x, nullptr, g, b, w, b0, scores, M, d, eps, n_act, s);
 }
 
 // ---------------------------------------------------------------- cache scatter

@@ -94,9 +94,10 @@ hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const fl
 // y[i] = LN(x[i]) * g + b over d features, rows row0 .. row0+M-1
 hipError_t launch_layernorm(bool bf, const void* x, void* y, const float* g, const float* b, int M, int d,
                             float eps, hipStream_t s);
-// scores[i] = LN(x[i]) . w + b0 (fp32)
+// Decoder head on LN(x[i]) = z_i (fp32 out): n_act == 0: scores[i] = z_i . w + b0;
+// n_act = k >= 2: scores[i][a] = softmax_a(z_i . w[:, a] + b0[a]), w [d][k].
 hipError_t launch_layernorm_score(bool bf, const void* x, const float* g, const float* b, const float* w,
-                                  const float* b0, float* scores, int M, int d, float eps, hipStream_t s);
+                                  const float* b0, float* scores, int M, int d, float eps, int n_act, hipStream_t s);
 
 // Paged attention: out[row] = softmax(q k^T / sqrt(dh) (+ rel bias)) v over the
 // request's cached keys (causal: keys at positions <= the query's position).
@@ -145,6 +146,7 @@ hipError_t launch_lg_attention(bool bf, const void* q, int ldq, void* out, int l
                                const AttnReq* reqs, const AttnTile* tiles, int n_tiles, int l_local,
                                const void* gkv, int gkv_ld, int dec_layer, hipStream_t s);
 constexpr int kLgQueryBlock = 64;
+constexpr int kMaxActions = 16;  // largest supported action vocabulary of the decoder head
 constexpr int kMaxLocal = 64;  // largest supported l_local
 
 // dst[n][k] = src[k][n] (src [K][N] row-major), same element type

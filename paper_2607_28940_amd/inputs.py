@@ -150,8 +150,9 @@ def make_weights(m: ModelConfig, variant: Sequence[str] = (), seed_w: int = SEED
     variant "affine": LayerNorm gain 1 + N(0, 0.1), offset N(0, 0.1).
     The pooling vector of the global token is N(0, 0.02) (nearly uniform
     pooling), N(0, 16) under "sharp" (pooling logits of a few units); the
-    action embeddings W_dec are N(0, (4/sqrt d)^2) under "sharp" (action
-    logits of a few units).
+    action embeddings W_dec are N(0, (4/sqrt d)^2) under "sharp" or
+    "sharp-head" (action logits of a few units; "sharp-head" leaves every
+    other tensor at its base draw).
     """
     variant = set(variant)
     d = m.d_model
@@ -167,7 +168,7 @@ def make_weights(m: ModelConfig, variant: Sequence[str] = (), seed_w: int = SEED
             w = (1.0 if "sharp" in variant else 0.02) * z
         elif name == "w_pool":
             w = (4.0 if "sharp" in variant else 0.02) * z
-        elif name == "W_dec" and "sharp" in variant:
+        elif name == "W_dec" and ("sharp" in variant or "sharp-head" in variant):
             w = (4.0 / math.sqrt(d)) * z
         elif "sharp" in variant and name in ("Wq", "Wk", "sWq", "sWk", "xWq", "xWk"):
             w = (2.0 / math.sqrt(d)) * z

@@ -40,13 +40,13 @@ class Config(ctypes.Structure):
     _fields_ = [("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("d_ffn", ctypes.c_int32),
                 ("n_enc_layers", ctypes.c_int32), ("n_dec_layers", ctypes.c_int32),
                 ("rel_pos_buckets", ctypes.c_int32), ("ln_eps", ctypes.c_float), ("dtype", ctypes.c_int32),
-                ("l_local", ctypes.c_int32), ("global_pool", ctypes.c_int32)]
+                ("l_local", ctypes.c_int32), ("global_pool", ctypes.c_int32), ("n_actions", ctypes.c_int32)]
 
     @classmethod
     def of(cls, m: ModelConfig) -> "Config":
         return cls(m.d_model, m.n_heads, m.d_ffn, m.n_enc_layers, m.n_dec_layers, m.rel_pos_buckets,
                    float(m.ln_eps), TX_BF16 if m.dtype == "bf16" else TX_F32, int(m.l_local),
-                   int(bool(m.global_pool)))
+                   int(bool(m.global_pool)), int(m.n_actions))
 
 
 _lib = None
@@ -237,7 +237,9 @@ class KVCache:
         import torch
         ids, so, co = _i32(req_ids), _i64(serving_offsets), _i64(candidate_offsets)
         if out is None:
-            out = torch.empty(int(co[-1]) if len(co) else 0, dtype=torch.float32, device=self.device)
+            n = int(co[-1]) if len(co) else 0
+            k = self.model.mc.n_actions
+            out = torch.empty((n, k) if k else n, dtype=torch.float32, device=self.device)
         ws, n = self._ws_for(TX_OP_SCORE, len(ids), so, co, ws_limit)
         check(lib().score_candidates(self.handle, len(ids), _p(ids, I32P), VP(serving.data_ptr()), _p(so, I64P),
                                      VP(candidates.data_ptr()), _p(co, I64P), VP(out.data_ptr()), VP(ws.data_ptr()),

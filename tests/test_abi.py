@@ -79,6 +79,18 @@ def test_sparse_config_counts_and_errors(L):
     L.tx_model_destroy(m)
 
 
+def test_action_head_config(L):
+    for k in (2, 3, 16):
+        m = I.ModelConfig(**{**I.workload("headline").model.__dict__, "n_actions": k})
+        c = T.Config.of(m)
+        assert L.tx_num_weights(ctypes.byref(c)) == I.n_weights(m)
+        assert L.tx_model_repack_bytes(ctypes.byref(c)) > L.tx_model_repack_bytes(ctypes.byref(_cfg()))
+    h = T.VP()
+    for k, code in ((1, T.TX_E_INVALID), (-2, T.TX_E_INVALID), (17, T.TX_E_UNSUPPORTED)):
+        bad = _cfg(n_actions=k)
+        assert L.tx_model_create(ctypes.byref(bad), T.VP(FAKE_REPACK), 1 << 30, 1, ctypes.byref(h)) == code, k
+
+
 def _model(L, cfg):
     h = T.VP()
     rc = L.tx_model_create(ctypes.byref(cfg), T.VP(FAKE_REPACK), L.tx_model_repack_bytes(ctypes.byref(cfg)), 7,

@@ -1,0 +1,104 @@
+"""Parity of the k-action query-key softmax decoder head (Sec. 4.1.3, Eq.
+action-decoding) on the GPU with the fp64 oracle, and its reduction to the
+scalar logit head: with two actions whose embeddings differ by w_s, the
+click probability is the logistic function of the scalar logit (the head is
+evaluated in fp32 on the same normalised row in both forms).
+
+The bf16 bar of 2e-2 is stated for scores, i.e. logits. Probabilities are a
+smooth function of the logits, so the bf16 cases compare in logit space: the
+centred log-probabilities (log p_a minus their mean over the actions, which
+is the logits minus their mean) under the same relative bar; with two actions
+this is exactly the scalar-logit criterion. The fp32 cases compare the
+probabilities themselves at 1e-4.
+
+The fp32 cases use the "sharp" variant throughout (they pin the head's
+indexing and softmax at 1e-4). The bf16 cases keep the configurations'
+weights for the decoder body and sharpen only the action embeddings
+("sharp-head"), so the probabilities stay far from uniform.
+
+The task states its bf16 bar (2e-2) for one scalar score per candidate; the
+k-action outputs have no stated bar, so it is derived: every logit carries the
+same bf16 error as a scalar score (the candidate representation's rounding
+projected on one embedding: sigma ~ 0.75e-2 relative, p99 1.3-1.5e-2 here,
+as for the scalar scores), and a case compares k times as many values. The
+bar is therefore the scalar one on the 99th percentile, p99 <= 2e-2, plus a
+maximum of 3e-2, the extreme-value allowance sqrt(2 ln N) * sigma ~ 3.9 sigma
+for the ~2,000 logits of a case (measured: 1.7e-2 at k = 3, 2.4e-2 at k = 16)."""
+import dataclasses
+
+import numpy as np
+import pytest
+from scipy.special import expit
+
+from paper_2607_28940_amd import inputs as I
+from paper_2607_28940_amd.inputs import ModelConfig
+from tests.parity_util import BF16_TOL, FP32_TOL, DeviceCase, log, oracle_request, score_err
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    torch.cuda.set_device(0)
+
+
+RAGGED = dict(L=[70, 200, 129, 1], S=[5, 0, 70, 3], C=[7, 100, 33, 1])
+SHARP, HEAD = ("sharp", "affine"), ("affine", "sharp-head")
+BF16_MULTI_MAX = 3e-2  # maximum over k logits per candidate (derivation above)
+CASES = [
+    ("f32-k3", ModelConfig(64, 2, 256, 1, 2, rel_pos_buckets=8, dtype="f32", n_actions=3), SHARP, FP32_TOL),
+    ("f32-dh64-k16", ModelConfig(128, 2, 256, 1, 2, rel_pos_buckets=8, dtype="f32", n_actions=16), SHARP, FP32_TOL),
+    ("f32-sparse-k5", ModelConfig(128, 2, 256, 1, 2, rel_pos_buckets=8, dtype="f32", n_actions=5, l_local=7,
+                                  global_pool=True), SHARP, FP32_TOL),
+    ("bf16-dh128-k3", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16, n_actions=3), HEAD, BF16_TOL),
+    ("bf16-dh64-k16", ModelConfig(256, 4, 512, 2, 2, rel_pos_buckets=16, n_actions=16), HEAD, BF16_TOL),
+    ("bf16-sparse-k4", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16, n_actions=4, l_local=10,
+                                   global_pool=True), HEAD, BF16_TOL),
+]
+
+
+@pytest.mark.parametrize("name,model,variant,tol", CASES, ids=[c[0] for c in CASES])
+def test_actions_vs_oracle(oracle_mod, name, model, variant, tol):
+    wl = I.custom_workload(model, cfg_id=61, **RAGGED)
+    w = I.make_weights(model, variant)
+    run = DeviceCase(wl, w)
+    run.build(range(wl.B))
+    g = run.score(range(wl.B))
+    orc = oracle_mod.Oracle(model, w)
+    o = [oracle_request(orc, wl, r)[0] for r in range(wl.B)]
+    G, Ob = np.concatenate(g), np.concatenate(o)
+    assert G.shape == Ob.shape == (sum(RAGGED["C"]), model.n_actions)
+    assert np.all(np.isfinite(G))
+    assert np.abs(G.sum(1) - 1).max() < 1e-5
+    assert float(G.max()) > 0.5  # far from uniform
+    if tol == FP32_TOL:
+        err = score_err(G.reshape(-1), Ob.reshape(-1))
+    else:
+        lg, lo = np.log(G), np.log(Ob)
+        err = score_err((lg - lg.mean(1, keepdims=True)).reshape(-1), (lo - lo.mean(1, keepdims=True)).reshape(-1))
+    log(f"actions {name}: max err {err['max']:.3e} p99 {err['p99']:.3e} (tol {tol})")
+    if tol == FP32_TOL:
+        assert err["max"] <= tol, err
+    else:
+        assert err["p99"] <= tol and err["max"] <= BF16_MULTI_MAX, err
+
+
+def test_two_actions_reduce_to_scalar_head():
+    m1 = ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16)
+    w1 = I.make_weights(m1, ("sharp", "affine"))
+    m2 = dataclasses.replace(m1, n_actions=2)
+    W2 = np.stack([w1[-2], np.zeros(m1.d_model, np.float32)], 1)
+    w2 = list(w1[:-2]) + [W2, np.array([w1[-1][0], 0.0], np.float32)]
+    wl1 = I.custom_workload(m1, cfg_id=62, **RAGGED)
+    wl2 = dataclasses.replace(wl1, model=m2)
+    r1, r2 = DeviceCase(wl1, w1), DeviceCase(wl2, w2)
+    r1.build(range(wl1.B))
+    r2.build(range(wl2.B))
+    s = np.concatenate(r1.score(range(wl1.B)))
+    P = np.concatenate(r2.score(range(wl2.B)))
+    e = float(np.abs(P[:, 0] - expit(s)).max())
+    log(f"two actions vs expit(scalar logit): {e:.3e}")
+    assert e < 1e-5
+    assert float(np.abs(P[:, 1] - expit(-s)).max()) < 1e-5
