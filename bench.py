@@ -10,6 +10,7 @@ resident in HBM when it starts. Prints one JSON line.
   python bench.py [--steps K] [--warmup W] [--workload headline]
   python bench.py --l-local 10        # local-global sparse cross-attention
                                       # (last 10 cached tokens + pooled token)
+  python bench.py --actions 3         # k-action softmax decoder head
 
 The JSON carries the roofline of the dominant kernel, whose per-launch time
 comes from HIP events the library records around each launch on the stream
@@ -61,7 +62,7 @@ def score_work(wl):
             f_gemm += (12 * d * d + 4 * d * F) * rows + (4 * d * d * S if last else 0)
             f_cross += 4.0 * cross_keys(m, L) * d * rows
             f_self += (0 if last else 2.0 * d * S * (S + 1)) + 4.0 * d * C * (S + 1)
-        f_gemm += 2 * d * C
+        f_gemm += 2 * d * C * max(1, m.n_actions)
     kv = sum(m.n_dec_layers * 2 * cross_keys(m, L) * d for L in wl.L) * es
     tok = sum(S + C for S, C in zip(wl.S, wl.C)) * d * es
     wts = m.n_dec_layers * (12 * d * d + 2 * d * F) * es
@@ -134,6 +135,8 @@ def main():
                     help="local-global sparse cross-attention window (0: dense cross-attention, the headline)")
     ap.add_argument("--no-global-token", action="store_true",
                     help="with --l-local: no attention-pooled global token")
+    ap.add_argument("--actions", type=int, default=0,
+                    help="k >= 2: softmax decoder head over k action tokens (0: the scalar logit head)")
     ap.add_argument("--cpu-requests", type=int, default=None,
                     help="requests in the oracle's timed sample (default: about 10 s of CPU work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -160,6 +163,8 @@ def main():
     if args.l_local > 0:
         wl = dataclasses.replace(wl, model=dataclasses.replace(wl.model, l_local=args.l_local,
                                                                global_pool=not args.no_global_token))
+    if args.actions:
+        wl = dataclasses.replace(wl, model=dataclasses.replace(wl.model, n_actions=args.actions))
     m = wl.model
     t_setup = time.time()
     weights = I.make_weights(m)
@@ -177,7 +182,8 @@ def main():
     xc = T.to_device(I.packed_tokens(wl, I.STREAM_CANDIDATES, threads=16), m)
     so, co = I.offsets(wl.S), I.offsets(wl.C)
     ids = list(range(wl.B))
-    out = torch.empty(int(co[-1]), dtype=torch.float32, device="cuda")
+    out = torch.empty((int(co[-1]), m.n_actions) if m.n_actions else int(co[-1]), dtype=torch.float32,
+                      device="cuda")
     torch.cuda.synchronize()
     print(f"# setup {time.time() - t_setup:.1f} s: {wl.B} caches built", file=sys.stderr, flush=True)
 
@@ -248,10 +254,13 @@ def main():
     if sparse:
         mode = f"local-global sparse cross-attention (last {m.l_local} cached tokens" + \
                (" + pooled global token)" if m.global_pool else ")")
-        metric = f"candidate scores/sec, {args.workload} with {mode} on 1 MI355X"
     else:
         mode = "dense cross-attention over every cached token"
-        metric = METRIC if args.workload == "headline" else f"candidate scores/sec, {args.workload} on 1 MI355X"
+    head = f"softmax over {m.n_actions} action tokens" if m.n_actions else "scalar logit head"
+    if sparse or m.n_actions or args.workload != "headline":
+        metric = f"candidate scores/sec, {args.workload} with {mode} and {head} on 1 MI355X"
+    else:
+        metric = METRIC
     line = {
         "metric": metric,
         "value": round(value, 1), "unit": "scores/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -261,7 +270,8 @@ def main():
                                f"S={'ragged' if len(set(wl.S)) > 1 else wl.S[0]} "
                                f"C={'ragged' if len(set(wl.C)) > 1 else wl.C[0]} d={m.d_model} H={m.n_heads} "
                                f"F={m.d_ffn} n_enc={m.n_enc_layers} n_dec={m.n_dec_layers} page=64",
-                   "global_batch": wl.B, "scores_per_step": n_scores, "cross_attention": mode},
+                   "global_batch": wl.B, "scores_per_step": n_scores, "cross_attention": mode,
+                   "head": head},
         "mfma_frac_of_peak": round(tflops / peak, 4),
         "achieved_tflops": round(tflops, 2),
         "algorithmic": {"flop_per_step": work["flop"], "bytes_per_step": work["bytes"]},

@@ -97,7 +97,7 @@ struct tx_model {
   float* wpool = nullptr;  // attention-pooling vector of the global token [d]
   int l_local = 0;         // > 0: local-global sparse cross-attention
   bool gpool = false;      // the sparse key set includes the pooled global token
-  int n_act = 0;           // 0: scalar logit head (ws [d], bs [1]); k: ws [d][k], bs [k]
+  int n_act = 0;           // 0: scalar logit head (ws [d], bs [1]); k: ws [k][d], bs [k]
   bool weights_set = false;
 };
 
@@ -279,7 +279,8 @@ int tx_model_set_weights(tx_model* m, const void* const* W, int32_t n_weights, h
   }
   const int hb = E_N * m->n_enc + D_N * m->n_dec;
   const int k = std::max(1, m->n_act);
-  run(bias(hb, m->ws, (int64_t)d * k));  // [d] or [d][k], kept in that order
+  if (m->n_act) run(launch_transpose_to_f32(bf, wp(hb), m->ws, d, k, stream));  // W_dec [d][k] -> [k][d]
+  else run(bias(hb, m->ws, d));
   run(bias(hb + 1, m->bs, k));
   if (m->gpool) run(bias(hb + 2, m->wpool, d));
   if (e != hipSuccess) return fail(TX_E_HIP, "weight repack launch failed: %s", hipGetErrorString(e));

@@ -9,12 +9,13 @@
 namespace tx {
 
 // Decoder head on one wave's row, given this lane's share of the normalised
-// row (z at features f(0..cnt-1), spaced by `stride` from c0). n_act == 0:
-// scores[row] = z . w + b0[0]. n_act = k >= 2: w is [d][k] (action a's
-// embedding in column a), lane a ends up with logit a, and the softmax over
-// the k lanes gives scores[row * k + a].
+// row (z at features c0 + e * stride, e < cnt). n_act == 0:
+// scores[row] = z . w + b0[0]. n_act = k >= 2: w is [k][d] (row a = action
+// a's embedding, repacked that way so a lane reads its features of one
+// action contiguously), lane a ends up with logit a, and the softmax over the
+// k lanes gives scores[row * k + a].
 template <int CNT>
-__device__ __forceinline__ void head_out(const float (&z)[CNT], int c0, int stride, int cnt, int lane,
+__device__ __forceinline__ void head_out(const float (&z)[CNT], int c0, int stride, int cnt, int lane, int d,
                                          const float* __restrict__ w, const float* __restrict__ b0,
                                          float* __restrict__ scores, int row, int n_act) {
   if (n_act == 0) {
@@ -32,7 +33,7 @@ __device__ __forceinline__ void head_out(const float (&z)[CNT], int c0, int stri
     float dot = 0.f;
 #pragma unroll
     for (int e = 0; e < CNT; ++e)
-      if (e < cnt) dot += z[e] * w[(size_t)(c0 + e * stride) * n_act + a];
+      if (e < cnt) dot += z[e] * w[(size_t)a * d + c0 + e * stride];
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) dot += __shfl_xor(dot, o);
     if (lane == a) mine = dot + b0[a];
@@ -80,7 +81,7 @@ __global__ __launch_bounds__(256) void layernorm_rows(const T* __restrict__ x, T
     float z[EPL];
 #pragma unroll
     for (int e = 0; e < EPL; ++e) z[e] = (v[e] - mean) * inv * g[c0 + e] + b[c0 + e];
-    head_out<EPL>(z, c0, 1, EPL, lane, w, b0, scores, row, n_act);
+    head_out<EPL>(z, c0, 1, EPL, lane, d, w, b0, scores, row, n_act);
   } else {
     T* yr = y + (size_t)row * d + c0;
 #pragma unroll
@@ -122,7 +123,7 @@ __global__ __launch_bounds__(256) void layernorm_rows_any(const T* __restrict__ 
     const int c = lane + 64 * e;
     z[e] = (e < cnt) ? ((float)xr[c] - mean) * inv * g[c] + b[c] : 0.f;
   }
-  head_out<MAXC>(z, lane, 64, cnt, lane, w, b0, scores, row, n_act);
+  head_out<MAXC>(z, lane, 64, cnt, lane, d, w, b0, scores, row, n_act);
 }
 
 template <typename T, bool SCORE>
@@ -266,6 +267,25 @@ hipError_t launch_transpose(bool bf, const void* src, void* dst, int K, int N, i
   dim3 grid((N + 31) / 32, (K + 31) / 32);
   if (bf) transpose_tiles<bf16><<<grid, 256, 0, s>>>((const bf16*)src, (bf16*)dst, K, N, dst_ld);
   else transpose_tiles<float><<<grid, 256, 0, s>>>((const float*)src, (float*)dst, K, N, dst_ld);
+  return hipGetLastError();
+}
+
+// dst fp32 [N][K] = src [K][N] (one-time repack of small matrices)
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_to_f32_kernel(const T* __restrict__ src, float* __restrict__ dst,
+                                                               int K, int N) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)K * N) return;
+  const int n = (int)(i / K), k = (int)(i % K);
+  dst[i] = (float)src[(size_t)k * N + n];
+}
+
+hipError_t launch_transpose_to_f32(bool bf, const void* src, float* dst, int K, int N, hipStream_t s) {
+  const int64_t n = (int64_t)K * N;
+  if (n <= 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((n + 255) / 256);
+  if (bf) transpose_to_f32_kernel<bf16><<<blocks, 256, 0, s>>>((const bf16*)src, dst, K, N);
+  else transpose_to_f32_kernel<float><<<blocks, 256, 0, s>>>((const float*)src, dst, K, N);
   return hipGetLastError();
 }
 

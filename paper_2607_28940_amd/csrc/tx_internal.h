@@ -95,7 +95,7 @@ hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const fl
 hipError_t launch_layernorm(bool bf, const void* x, void* y, const float* g, const float* b, int M, int d,
                             float eps, hipStream_t s);
 // Decoder head on LN(x[i]) = z_i (fp32 out): n_act == 0: scores[i] = z_i . w + b0;
-// n_act = k >= 2: scores[i][a] = softmax_a(z_i . w[:, a] + b0[a]), w [d][k].
+// n_act = k >= 2: scores[i][a] = softmax_a(z_i . w[a] + b0[a]), w fp32 [k][d].
 hipError_t launch_layernorm_score(bool bf, const void* x, const float* g, const float* b, const float* w,
                                   const float* b0, float* scores, int M, int d, float eps, int n_act, hipStream_t s);
 
@@ -151,6 +151,8 @@ constexpr int kMaxLocal = 64;  // largest supported l_local
 
 // dst[n][k] = src[k][n] (src [K][N] row-major), same element type
 hipError_t launch_transpose(bool bf, const void* src, void* dst, int K, int N, int dst_ld, hipStream_t s);
+// dst fp32 [N][K] = src [K][N]
+hipError_t launch_transpose_to_f32(bool bf, const void* src, float* dst, int K, int N, hipStream_t s);
 // dst fp32[n] = src[n]
 hipError_t launch_to_f32(bool bf, const void* src, float* dst, int64_t n, hipStream_t s);
 
