@@ -190,6 +190,19 @@ class Oracle:
             rows = np.concatenate([rows, self.pool(Henc)[None, :]], 0)
         return rows
 
+    def run_events(self, Xb, events):
+        """Event-sliced forward of one user (Sec. 4.2, single-pass seq-to-seq
+        training; causal attention and prefix reuse): the behavior stream is
+        encoded once, and serving event t = (p_t, Xs_t, Xc_t) is decoded
+        against the cross K/V of the first p_t encoded rows only (its prefix
+        H_<t). Returns the list of per-event scores."""
+        H, _, _, _ = self.encode(Xb)
+        out = []
+        for p, Xs, Xc in events:
+            Kx, Vx = self.cross_kv(self.key_rows(H[:p]))
+            out.append(self.score(Kx, Vx, Xs, Xc))
+        return out
+
     def run_request(self, Xb, Xs, Xc, Xev=None):
         """Whole path for one request: encode behavior (then append events if
         given), project cross K/V of the rows the cross-attention sees, decode,
