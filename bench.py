@@ -11,6 +11,9 @@ resident in HBM when it starts. Prints one JSON line.
   python bench.py --l-local 10        # local-global sparse cross-attention
                                       # (last 10 cached tokens + pooled token)
   python bench.py --actions 3         # k-action softmax decoder head
+  python bench.py --events 8          # event-sliced decoding (seq2seq training
+                                      # forward): B/8 users x 8 serving events,
+                                      # each against its own prefix of the cache
 
 The JSON carries the roofline of the dominant kernel, whose per-launch time
 comes from HIP events the library records around each launch on the stream
@@ -135,6 +138,8 @@ def main():
                     help="local-global sparse cross-attention window (0: dense cross-attention, the headline)")
     ap.add_argument("--no-global-token", action="store_true",
                     help="with --l-local: no attention-pooled global token")
+    ap.add_argument("--events", type=int, default=0,
+                    help="T > 0: B/T users with T serving events each, decoded against prefixes L(t+1)/T")
     ap.add_argument("--actions", type=int, default=0,
                     help="k >= 2: softmax decoder head over k action tokens (0: the scalar logit head)")
     ap.add_argument("--cpu-requests", type=int, default=None,
@@ -169,12 +174,15 @@ def main():
     t_setup = time.time()
     weights = I.make_weights(m)
     model = T.Model(m, weights)
-    n_pages = sum((L + 63) // 64 for L in wl.L)
-    cache = T.KVCache(model, n_pages=n_pages, max_requests=wl.B, max_tokens=max(wl.L))
-    # build every request's cache (untimed), a few requests at a time
+    # caches of the users (every request, or B/T users with T events each)
+    n_users = max(1, wl.B // args.events) if args.events else wl.B
+    users = list(range(n_users))
+    n_pages = sum((wl.L[u] + 63) // 64 for u in users)
+    cache = T.KVCache(model, n_pages=n_pages, max_requests=n_users, max_tokens=max(wl.L))
+    # build every user's cache (untimed), a few at a time
     chunk = max(1, (1 << 19) // max(1, max(wl.L)))
-    for a in range(0, wl.B, chunk):
-        ids = list(range(a, min(wl.B, a + chunk)))
+    for a in range(0, n_users, chunk):
+        ids = list(range(a, min(n_users, a + chunk)))
         Xb = T.to_device(I.packed_tokens(wl, I.STREAM_BEHAVIOR, ids, threads=16), m)
         cache.build(ids, Xb, I.offsets([wl.L[r] for r in ids]), ws_limit=8 << 30)
         del Xb
@@ -182,10 +190,23 @@ def main():
     xc = T.to_device(I.packed_tokens(wl, I.STREAM_CANDIDATES, threads=16), m)
     so, co = I.offsets(wl.S), I.offsets(wl.C)
     ids = list(range(wl.B))
+    prefix = None
+    if args.events:
+        # serving event e = t of user u = e // T, decoded against the first
+        # L (t + 1) / T cached tokens; the work model counts those prefixes
+        ids = [min(e // args.events, n_users - 1) for e in range(wl.B)]
+        prefix = [max(1, wl.L[ids[e]] * (e % args.events + 1) // args.events) for e in range(wl.B)]
+        wl = dataclasses.replace(wl, L=prefix)
+
+    def step():
+        if prefix is None:
+            cache.score(ids, xs, so, xc, co, out=out)
+        else:
+            cache.score_events(ids, prefix, xs, so, xc, co, out=out)
     out = torch.empty((int(co[-1]), m.n_actions) if m.n_actions else int(co[-1]), dtype=torch.float32,
                       device="cuda")
     torch.cuda.synchronize()
-    print(f"# setup {time.time() - t_setup:.1f} s: {wl.B} caches built", file=sys.stderr, flush=True)
+    print(f"# setup {time.time() - t_setup:.1f} s: {n_users} caches built", file=sys.stderr, flush=True)
 
     if args.calib_copy:
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
@@ -194,7 +215,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     for _ in range(args.warmup):
-        cache.score(ids, xs, so, xc, co, out=out)
+        step()
     torch.cuda.synchronize()
     if not args.no_profile:
         T.profile_enable(True)
@@ -203,7 +224,7 @@ def main():
     torch.cuda.synchronize()
     ev0.record(stream)
     for _ in range(args.steps):
-        cache.score(ids, xs, so, xc, co, out=out)
+        step()
     ev1.record(stream)
     torch.cuda.synchronize()
     ms = ev0.elapsed_time(ev1) / args.steps
@@ -257,7 +278,11 @@ def main():
     else:
         mode = "dense cross-attention over every cached token"
     head = f"softmax over {m.n_actions} action tokens" if m.n_actions else "scalar logit head"
-    if sparse or m.n_actions or args.workload != "headline":
+    if args.events:
+        metric = (f"candidate scores/sec, event-sliced decoding (seq2seq training forward): {n_users} users x "
+                  f"{args.events} serving events of the {args.workload} shape, each against its own cache prefix, "
+                  f"with {mode} and {head} on 1 MI355X")
+    elif sparse or m.n_actions or args.workload != "headline":
         metric = f"candidate scores/sec, {args.workload} with {mode} and {head} on 1 MI355X"
     else:
         metric = METRIC
@@ -271,7 +296,9 @@ def main():
                                f"C={'ragged' if len(set(wl.C)) > 1 else wl.C[0]} d={m.d_model} H={m.n_heads} "
                                f"F={m.d_ffn} n_enc={m.n_enc_layers} n_dec={m.n_dec_layers} page=64",
                    "global_batch": wl.B, "scores_per_step": n_scores, "cross_attention": mode,
-                   "head": head},
+                   "head": head,
+                   "events": ({"users": n_users, "per_user": args.events,
+                               "prefixes": "L (t + 1) / T"} if args.events else None)},
         "mfma_frac_of_peak": round(tflops / peak, 4),
         "achieved_tflops": round(tflops, 2),
         "algorithmic": {"flop_per_step": work["flop"], "bytes_per_step": work["bytes"]},

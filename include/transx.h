@@ -11,6 +11,8 @@
  *   kv_cache_build    encode behavior sequences, fill the paged per-request cache
  *   kv_cache_append   encode only newly appended events against the cached prefix
  *   score_candidates  decoder over serving + candidate tokens, linear head
+ *   score_events      the same per serving event of a user, each against its
+ *                     own prefix of the cache (seq-to-seq training forward)
  *
  * Conventions
  *   - All tensors the caller hands over are device pointers unless marked
@@ -230,6 +232,22 @@ int score_candidates(const tx_kv_cache* cache, int32_t n_req, const int32_t* req
                      const void* serving, const int64_t* serving_offsets /* host */, const void* candidates,
                      const int64_t* candidate_offsets /* host */, float* scores, void* ws, size_t ws_bytes,
                      hipStream_t stream);
+
+/* score_events -- event-sliced decoding for seq-to-seq training (Sec. 4.2:
+ * the behavior stream is encoded once and every serving event decodes against
+ * its own prefix of it, sliced rather than re-encoded; exact because the
+ * encoder is causal). Event e uses the cache of request req_ids[e] (ids may
+ * repeat: several events of one user) but only its first prefix_len[e]
+ * cached tokens as cross-attention keys (1 <= prefix_len[e] <= cached length).
+ * With the local-global sparse form the window is the prefix's last l_local
+ * tokens; a pooled global token exists only for the whole history, so with
+ * global_pool every prefix_len[e] must equal the cached length
+ * (TX_E_UNSUPPORTED otherwise). Other arguments, outputs and errors as in
+ * score_candidates, with events in place of requests. */
+int score_events(const tx_kv_cache* cache, int32_t n_events, const int32_t* req_ids /* host */,
+                 const int64_t* prefix_len /* host */, const void* serving, const int64_t* serving_offsets /* host */,
+                 const void* candidates, const int64_t* candidate_offsets /* host */, float* scores, void* ws,
+                 size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------ measurement */
 

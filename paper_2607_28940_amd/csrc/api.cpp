@@ -1020,8 +1020,11 @@ int kv_cache_append(tx_kv_cache* c, int32_t n, const int32_t* ids, const void* X
 // ------------------------------------------------------------------ score
 namespace {
 
-int run_score_pass(const tx_kv_cache* c, const int32_t* ids, int a, int b, const char* xs, const int64_t* so,
-                   const char* xc, const int64_t* co, float* scores, char* ws, hipStream_t st) {
+// Decoder + head over groups a .. b-1 (a group = one serving event: its
+// serving and candidate rows, decoded against the first kvlen[r] cached
+// tokens of request ids[r]).
+int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvlen, int a, int b, const char* xs,
+                   const int64_t* so, const char* xc, const int64_t* co, float* scores, char* ws, hipStream_t st) {
   const tx_model* m = c->m;
   const bool bf = m->bf;
   const int d = m->d, F = m->F, H = m->H;
@@ -1037,7 +1040,7 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, int a, int b, const
     const int r = a + i;
     const int S = (int)(so[r + 1] - so[r]), C = (int)(co[r + 1] - co[r]);
     const int s_row = (int)(so[r] - so[a]), c_row = (int)(Ms + co[r] - co[a]);
-    const int kv = (int)c->len[ids[r]];
+    const int kv = (int)kvlen[r];
     sreq[i] = SelfReq{s_row, S, c_row, C};
     full[i] = AttnReq{s_row, S, c_row, C, kv, 0, ids[r], 0};
     cand[i] = AttnReq{c_row, C, 0, 0, kv, 0, ids[r], 0};
@@ -1144,6 +1147,27 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, int a, int b, const
   return TX_OK;
 }
 
+// Shared by score_candidates and score_events once ids and key lengths are
+// checked: offsets, pointers, workspace, then the passes.
+int score_groups(const tx_kv_cache* c, int n, const int32_t* ids, const int64_t* kvlen, const void* serving,
+                 const int64_t* so, const void* cand, const int64_t* co, float* scores, void* ws, size_t ws_bytes,
+                 hipStream_t st) {
+  TX_CHECK(check_offsets(so, n, "serving", 0));
+  TX_CHECK(check_offsets(co, n, "candidate", 0));
+  TX_CHECK(check_tokens(c, n, serving, so, "serving"));
+  TX_CHECK(check_tokens(c, n, cand, co, "candidate"));
+  if (co[n] > co[0] && !scores) return fail(TX_E_INVALID, "scores pointer is null");
+  if (((uintptr_t)scores & 3)) return fail(TX_E_INVALID, "scores pointer misaligned");
+  std::vector<int> cuts;
+  TX_CHECK(plan_passes(c->m, TX_OP_SCORE, n, so, co, ws_bytes, cuts));
+  if (!ws) return fail(TX_E_INVALID, "workspace is null");
+  TX_CHECK(check_weights(c));
+  for (size_t p = 0; p + 1 < cuts.size(); ++p)
+    TX_CHECK(run_score_pass(c, ids, kvlen, cuts[p], cuts[p + 1], (const char*)serving, so, (const char*)cand, co,
+                            scores, (char*)ws, st));
+  return TX_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1152,22 +1176,33 @@ int score_candidates(const tx_kv_cache* c, int32_t n, const int32_t* ids, const 
                      const void* cand, const int64_t* co, float* scores, void* ws, size_t ws_bytes, hipStream_t st) {
   TX_CHECK(common_checks(c, n, ids, ws));
   if (n == 0) return TX_OK;
-  TX_CHECK(check_offsets(so, n, "serving", 0));
-  TX_CHECK(check_offsets(co, n, "candidate", 0));
-  TX_CHECK(check_tokens(c, n, serving, so, "serving"));
-  TX_CHECK(check_tokens(c, n, cand, co, "candidate"));
-  if (co[n] > co[0] && !scores) return fail(TX_E_INVALID, "scores pointer is null");
-  if (((uintptr_t)scores & 3)) return fail(TX_E_INVALID, "scores pointer misaligned");
-  for (int i = 0; i < n; ++i)
+  std::vector<int64_t> kvlen(n);
+  for (int i = 0; i < n; ++i) {
     if (c->len[ids[i]] < 1) return fail(TX_E_NOCACHE, "request %d has no cache", ids[i]);
-  std::vector<int> cuts;
-  TX_CHECK(plan_passes(c->m, TX_OP_SCORE, n, so, co, ws_bytes, cuts));
-  if (!ws) return fail(TX_E_INVALID, "workspace is null");
-  TX_CHECK(check_weights(c));
-  for (size_t p = 0; p + 1 < cuts.size(); ++p)
-    TX_CHECK(run_score_pass(c, ids, cuts[p], cuts[p + 1], (const char*)serving, so, (const char*)cand, co, scores,
-                            (char*)ws, st));
-  return TX_OK;
+    kvlen[i] = c->len[ids[i]];
+  }
+  return score_groups(c, n, ids, kvlen.data(), serving, so, cand, co, scores, ws, ws_bytes, st);
+}
+
+int score_events(const tx_kv_cache* c, int32_t n, const int32_t* ids, const int64_t* prefix, const void* serving,
+                 const int64_t* so, const void* cand, const int64_t* co, float* scores, void* ws, size_t ws_bytes,
+                 hipStream_t st) {
+  if (!c) return fail(TX_E_INVALID, "cache is null");
+  if (n < 0) return fail(TX_E_INVALID, "n_events %d", n);
+  if (n == 0) return TX_OK;
+  if (!ids || !prefix) return fail(TX_E_INVALID, "event ids or prefix lengths are null");
+  if (((uintptr_t)ws & 255)) return fail(TX_E_INVALID, "workspace not 256-byte aligned");
+  for (int i = 0; i < n; ++i) {
+    if (ids[i] < 0 || ids[i] >= c->max_req) return fail(TX_E_INVALID, "request id %d out of range", ids[i]);
+    if (c->len[ids[i]] < 1) return fail(TX_E_NOCACHE, "request %d has no cache", ids[i]);
+    if (prefix[i] < 1 || prefix[i] > c->len[ids[i]])
+      return fail(TX_E_INVALID, "event %d: prefix %lld outside 1 .. %lld", i, (long long)prefix[i],
+                  (long long)c->len[ids[i]]);
+    if (c->m->gpool && prefix[i] != c->len[ids[i]])
+      return fail(TX_E_UNSUPPORTED, "event %d: the pooled global token is kept for the whole cached history only",
+                  i);
+  }
+  return score_groups(c, n, ids, prefix, serving, so, cand, co, scores, ws, ws_bytes, st);
 }
 
 }  // extern "C"

@@ -77,6 +77,7 @@ _SIGS = {
     "kv_cache_build": (ctypes.c_int, [VP, ctypes.c_int32, I32P, VP, I64P, VP, ctypes.c_size_t, VP]),
     "kv_cache_append": (ctypes.c_int, [VP, ctypes.c_int32, I32P, VP, I64P, VP, ctypes.c_size_t, VP]),
     "score_candidates": (ctypes.c_int, [VP, ctypes.c_int32, I32P, VP, I64P, VP, I64P, VP, VP, ctypes.c_size_t, VP]),
+    "score_events": (ctypes.c_int, [VP, ctypes.c_int32, I32P, I64P, VP, I64P, VP, I64P, VP, VP, ctypes.c_size_t, VP]),
     "tx_profile_enable": (ctypes.c_int, [ctypes.c_int32]),
     "tx_profile_classes": (ctypes.c_int32, []),
     "tx_profile_class_name": (ctypes.c_char_p, [ctypes.c_int32]),
@@ -244,6 +245,22 @@ class KVCache:
         check(lib().score_candidates(self.handle, len(ids), _p(ids, I32P), VP(serving.data_ptr()), _p(so, I64P),
                                      VP(candidates.data_ptr()), _p(co, I64P), VP(out.data_ptr()), VP(ws.data_ptr()),
                                      n, VP(_stream(stream))))
+        return out
+
+    def score_events(self, req_ids, prefix_len, serving, serving_offsets, candidates, candidate_offsets, out=None,
+                     stream=None, ws_limit: Optional[int] = None):
+        """Event-sliced decoding: event e decodes against the first
+        prefix_len[e] cached tokens of request req_ids[e] (ids may repeat)."""
+        import torch
+        ids, pre, so, co = _i32(req_ids), _i64(prefix_len), _i64(serving_offsets), _i64(candidate_offsets)
+        if out is None:
+            n = int(co[-1]) if len(co) else 0
+            k = self.model.mc.n_actions
+            out = torch.empty((n, k) if k else n, dtype=torch.float32, device=self.device)
+        ws, n = self._ws_for(TX_OP_SCORE, len(ids), so, co, ws_limit)
+        check(lib().score_events(self.handle, len(ids), _p(ids, I32P), _p(pre, I64P), VP(serving.data_ptr()),
+                                 _p(so, I64P), VP(candidates.data_ptr()), _p(co, I64P), VP(out.data_ptr()),
+                                 VP(ws.data_ptr()), n, VP(_stream(stream))))
         return out
 
     def release(self, req_ids):

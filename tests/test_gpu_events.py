@@ -1,0 +1,112 @@
+"""Event-sliced decoding on the GPU (score_events) against the fp64 oracle
+(Sec. 4.2: one encoding of the behavior stream, every serving event decoded
+against its own prefix of it). Prefixes at and around page boundaries,
+several users with interleaved events (repeated request ids), the sparse
+local window inside the prefix, the action head; full-length events equal
+score_candidates bitwise; invalid prefixes are rejected on the host."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from paper_2607_28940_amd import inputs as I
+from paper_2607_28940_amd import transx as T
+from paper_2607_28940_amd.inputs import ModelConfig
+from tests.parity_util import BF16_TOL, FP32_TOL, DeviceCase, log, score_err
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    torch.cuda.set_device(0)
+
+
+USERS_L = [200, 70]
+# (user, prefix, S, C)
+EVENTS = [(0, 1, 3, 5), (1, 9, 0, 7), (0, 63, 4, 9), (0, 64, 2, 4), (1, 70, 6, 3), (0, 65, 70, 11),
+          (0, 130, 1, 33), (1, 64, 2, 2), (0, 200, 5, 6)]
+
+
+def _setup(m, variant, cfg_id):
+    wl = I.custom_workload(m, USERS_L, [1] * len(USERS_L), [1] * len(USERS_L), cfg_id=cfg_id)
+    w = I.make_weights(m, variant)
+    run = DeviceCase(wl, w)
+    run.build(range(len(USERS_L)))
+    ewl = I.custom_workload(m, [1] * len(EVENTS), [e[2] for e in EVENTS], [e[3] for e in EVENTS], cfg_id=cfg_id + 1)
+    Xs = [I.request_tokens(ewl, t, I.STREAM_SERVING) for t in range(len(EVENTS))]
+    Xc = [I.request_tokens(ewl, t, I.STREAM_CANDIDATES) for t in range(len(EVENTS))]
+    return wl, w, run, Xs, Xc
+
+
+def _gpu_events(run, Xs, Xc, events=EVENTS):
+    d = run.m.d_model
+    so, co = I.offsets([len(x) for x in Xs]), I.offsets([len(x) for x in Xc])
+    xs = run.dev(np.concatenate(Xs) if sum(map(len, Xs)) else np.zeros((1, d), np.float32))
+    xc = run.dev(np.concatenate(Xc))
+    out = run.cache.score_events([e[0] for e in events], [e[1] for e in events], xs, so, xc, co)
+    run.torch.cuda.synchronize()
+    s = out.cpu().numpy().astype(np.float64)
+    return [s[co[t]:co[t + 1]] for t in range(len(events))]
+
+
+def _oracle_events(orc, wl, Xs, Xc):
+    out = [None] * len(EVENTS)
+    for u in range(len(USERS_L)):
+        Xb = I.request_tokens(wl, u, I.STREAM_BEHAVIOR)
+        idx = [t for t, e in enumerate(EVENTS) if e[0] == u]
+        got = orc.run_events(Xb, [(EVENTS[t][1], Xs[t], Xc[t]) for t in idx])
+        for t, g in zip(idx, got):
+            out[t] = g
+    return out
+
+
+CASES = [
+    ("f32", ModelConfig(64, 2, 256, 1, 2, rel_pos_buckets=8, dtype="f32"), ("sharp", "affine"), FP32_TOL),
+    ("bf16-dh128", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16), ("sharp", "affine"), BF16_TOL),
+    ("bf16-dh64-local5", ModelConfig(256, 4, 512, 2, 2, rel_pos_buckets=16, l_local=5), ("sharp", "affine"),
+     BF16_TOL),
+    ("f32-k3", ModelConfig(64, 2, 256, 1, 2, rel_pos_buckets=8, dtype="f32", n_actions=3), ("sharp", "affine"),
+     FP32_TOL),
+]
+
+
+@pytest.mark.parametrize("name,model,variant,tol", CASES, ids=[c[0] for c in CASES])
+def test_events_vs_oracle(oracle_mod, name, model, variant, tol):
+    wl, w, run, Xs, Xc = _setup(model, variant, cfg_id=81)
+    g = _gpu_events(run, Xs, Xc)
+    o = _oracle_events(oracle_mod.Oracle(model, w), wl, Xs, Xc)
+    G, O = np.concatenate(g).reshape(-1), np.concatenate(o).reshape(-1)
+    assert np.all(np.isfinite(G))
+    err = score_err(G, O)
+    log(f"events {name}: max err {err['max']:.3e} p99 {err['p99']:.3e} (tol {tol})")
+    assert err["max"] <= tol, err
+
+
+def test_full_prefix_events_equal_score_candidates():
+    m = ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16)
+    wl, w, run, Xs, Xc = _setup(m, ("sharp", "affine"), cfg_id=83)
+    ev = [(0, 200, 4, 9), (1, 70, 6, 3)]
+    Xs2, Xc2 = Xs[:2], Xc[:2]
+    g = _gpu_events(run, Xs2, Xc2, ev)
+    d = m.d_model
+    so, co = I.offsets([len(x) for x in Xs2]), I.offsets([len(x) for x in Xc2])
+    out = run.cache.score([0, 1], run.dev(np.concatenate(Xs2)), so, run.dev(np.concatenate(Xc2)), co)
+    run.torch.cuda.synchronize()
+    s = out.cpu().numpy().astype(np.float64)
+    assert np.array_equal(np.concatenate(g), s)
+
+
+def test_event_prefix_errors():
+    m = ModelConfig(64, 2, 256, 1, 1, rel_pos_buckets=8, dtype="f32", l_local=4, global_pool=True)
+    wl, w, run, Xs, Xc = _setup(m, (), cfg_id=85)
+    for ev, code in (([(0, 0, 3, 5)], T.TX_E_INVALID), ([(0, 201, 3, 5)], T.TX_E_INVALID),
+                     ([(0, 120, 3, 5)], T.TX_E_UNSUPPORTED), ([(5, 10, 3, 5)], T.TX_E_INVALID)):
+        with pytest.raises(T.TxError) as e:
+            _gpu_events(run, Xs[:1], Xc[:1], ev)
+        assert e.value.code == code, (ev, e.value)
+    # the whole history is fine with the pooled token
+    g = _gpu_events(run, Xs[:1], Xc[:1], [(0, 200, 3, 5)])
+    assert np.all(np.isfinite(g[0]))
