@@ -49,7 +49,21 @@ struct MfmaAcc {
 // raw logit goes through `mask(key, s)`, which returns it (plus any bias, in
 // raw units) or -inf; other tiles skip that work. The O^T rescale is skipped when no lane's
 // max moved.
-template <int DH, int KLD, int VLD, class Mask>
+// LDS addresses of the MFMA fragments. Padded tiles: K rows of KLD elements,
+// V^T rows of VLD. Swizzled tiles (SWZ, filled by direct-to-LDS loads): K
+// rows of DH elements with 16-byte slot s of row r holding chunk s ^ (r mod
+// DH/8), V^T rows of 64 with slot s holding chunk s ^ ((r / 2) mod 8); both
+// keep the fragment reads of 8 consecutive rows on distinct banks.
+template <int DH, int KLD, bool SWZ>
+__device__ __forceinline__ int k_frag(int row, int slot) {
+  return SWZ ? row * DH + ((slot ^ (row & (DH / 8 - 1))) << 3) : row * KLD + (slot << 3);
+}
+template <int VLD, bool SWZ>
+__device__ __forceinline__ int v_frag(int row, int slot) {
+  return SWZ ? row * 64 + ((slot ^ ((row >> 1) & 7)) << 3) : row * VLD + (slot << 3);
+}
+
+template <int DH, int KLD, int VLD, class Mask, bool SWZ = false>
 __device__ __forceinline__ void mfma_attend_tile(const bf16* __restrict__ sK, const bf16* __restrict__ sV,
                                                  const bf16x8 (&qf)[DH / 16], MfmaAcc<DH>& acc, float scale_log2,
                                                  int l32, int hi, bool masked, Mask mask) {
@@ -60,7 +74,7 @@ __device__ __forceinline__ void mfma_attend_tile(const bf16* __restrict__ sK, co
     for (int v = 0; v < 16; ++v) s[kb][v] = 0.f;
 #pragma unroll
     for (int kk = 0; kk < DH / 16; ++kk) {
-      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&sK[(kb * 32 + l32) * KLD + 16 * kk + 8 * hi]);
+      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&sK[k_frag<DH, KLD, SWZ>(kb * 32 + l32, 2 * kk + hi)]);
       s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
     }
   }
@@ -121,7 +135,7 @@ __device__ __forceinline__ void mfma_attend_tile(const bf16* __restrict__ sK, co
     const int kbase = kb * 32 + 16 * half + 8 * hi;  // in the V^T tile's permuted key order
 #pragma unroll
     for (int db = 0; db < DH / 32; ++db) {
-      const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&sV[(32 * db + l32) * VLD + kbase]);
+      const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&sV[v_frag<VLD, SWZ>(32 * db + l32, kbase >> 3)]);
       acc.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc.o[db], 0, 0, 0);
     }
   }
@@ -147,10 +161,13 @@ __device__ __forceinline__ void mfma_store_out(const MfmaAcc<DH>& acc, bf16* __r
 //
 // A block of 4 waves serves up to 128 queries of one (request, head); each
 // wave owns 32 queries. For every 64-token page the block stages K [64][dh]
-// and V^T [dh][64] in LDS (double-buffered; the next two pages travel from HBM
-// in registers while the current one is used), so every K/V byte fetched from
-// HBM/L2 feeds all queries of the block. The page keeps V^T in the column
-// order the PV MFMA wants, so both tiles go to LDS as plain 16-byte stores.
+// and V^T [dh][64] in LDS (double-buffered: the next page travels from HBM/L2
+// straight into LDS with global_load_lds while the current one is used, no
+// register staging), so every K/V byte fetched from HBM/L2 feeds all queries
+// of the block. The page keeps V^T in the column order the PV MFMA wants; the
+// tiles are XOR-swizzled in LDS (the swizzle applied on the global side, since
+// each lane's 16 bytes land at a fixed slot) so fragment reads are
+// bank-conflict free without padding.
 //
 // Per wave and page:  S^T = K Q^T  (v_mfma_f32_32x32x16_bf16, keys as rows so
 // that a lane holds 32 keys of one query: the softmax row reduction is within
@@ -169,11 +186,9 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
                                                            PageGeom g, int layer_slot, const AttnReq* __restrict__ reqs,
                                                            const AttnTile* __restrict__ tiles,
                                                            const float* __restrict__ rel, int R, float scale_log2) {
-  constexpr int KLD = DH + 8;  // LDS row stride of K (elements)
-  constexpr int VLD = 64 + 8;  // LDS row stride of V^T
-  constexpr int NCH = 64 * DH / 8 / 256;  // 16-byte chunks per thread per slab
-  __shared__ __attribute__((aligned(16))) bf16 sK[2][64 * KLD];
-  __shared__ __attribute__((aligned(16))) bf16 sV[2][DH * VLD];
+  constexpr int KLD = DH, VLD = 64;  // swizzled, unpadded tiles
+  __shared__ __attribute__((aligned(16))) bf16 sK0[64 * DH], sK1[64 * DH];
+  __shared__ __attribute__((aligned(16))) bf16 sV0[DH * 64], sV1[DH * 64];
 
   const AttnTile tile = tiles[blockIdx.x];
   if (tile.q_count <= 0) return;
@@ -209,41 +224,47 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
   }
   const int32_t* ptab = page_table + (size_t)rq.slot * max_pages;
 
-  // Two register sets carry pages p+1 and p+2 from HBM while page p is used
-  // from LDS, so a load has two pages of compute to arrive.
-  bf16x8 ka[NCH], va[NCH], kb[NCH], vb[NCH];
-  auto gload = [&](int p, bf16x8 (&rk)[NCH], bf16x8 (&rv)[NCH]) {
-    // past the last page the last page is fetched again (unconditional loads
-    // keep the wait before each LDS store down to the older register set)
-    const size_t base = (size_t)ptab[min(p, n_pages - 1)] * g.page_elems;
-    const bf16x8* kp = reinterpret_cast<const bf16x8*>(pool + base + g.k_off(layer_slot, h));
-    const bf16x8* vp = reinterpret_cast<const bf16x8*>(pool + base + g.v_off(layer_slot, h));
+  // Pages travel HBM/L2 -> LDS with global_load_lds_dwordx4: each wave moves
+  // DH/32 KB of the K slab and as much of the V^T slab per page; lane l of a
+  // 1 KB load fills 16-byte slot l of it with the chunk the swizzle puts there.
+  // Page p+1 is requested while page p is used; every wave waits for its own
+  // loads before the page's closing barrier.
+  typedef __attribute__((address_space(3))) void* lds_ptr_t;
+  auto dma = [&](int p, bf16* dK, bf16* dV) {
+    const bf16* base = pool + (size_t)ptab[p] * g.page_elems;
+    const bf16* kp = base + g.k_off(layer_slot, h);
+    const bf16* vp = base + g.v_off(layer_slot, h);
 #pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      rk[u] = kp[tid + 256 * u];
-      rv[u] = vp[tid + 256 * u];
+    for (int u = 0; u < DH / 32; ++u) {
+      const int gi = wave * (DH / 32) + u;      // 1 KB piece of the slab
+      const int e = gi * 512 + lane * 8;        // its lane's first element
+      const int kr = e / DH, ks = (e % DH) >> 3;
+      __builtin_amdgcn_global_load_lds(kp + kr * DH + ((ks ^ (kr & (DH / 8 - 1))) << 3),
+                                       (lds_ptr_t)(dK + gi * 512), 16, 0, 0);
+      const int vr = e >> 6, vs = (e & 63) >> 3;
+      __builtin_amdgcn_global_load_lds(vp + vr * 64 + ((vs ^ ((vr >> 1) & 7)) << 3), (lds_ptr_t)(dV + gi * 512),
+                                       16, 0, 0);
     }
   };
-  auto lstore = [&](int buf, int p, const bf16x8 (&rk)[NCH], const bf16x8 (&rv)[NCH]) {
-    const int valid = kv_len - p * kPage;  // keys of this page that exist (may exceed 64)
-#pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const int e = (tid + 256 * u) * 8;
-      *reinterpret_cast<bf16x8*>(&sK[buf][(e / DH) * KLD + (e % DH)]) = rk[u];
-      const int vr = e >> 6, vc = e & 63;  // V^T row (feature) and first stored column of the chunk
-      bf16x8 vv = rv[u];
-      if (valid < kPage) {  // only the request's last page is partial (uniform branch)
-#pragma unroll
-        for (int t = 0; t < 8; ++t)
-          if (vt_col(vc + t) >= valid) vv[t] = (bf16)0.f;
-      }
-      *reinterpret_cast<bf16x8*>(&sV[buf][vr * VLD + vc]) = vv;
+  // keys past the request's length on its last page: V^T columns zeroed in LDS
+  // (the page may hold anything there; their K logits are masked anyway)
+  auto zero_tail = [&](int p, bf16* dV) {
+    const int valid = kv_len - p * kPage;
+    for (int e = tid; e < DH * 64; e += 256) {
+      const int r = e >> 6, col = e & 63;
+      const int chunk = (col >> 3) ^ ((r >> 1) & 7);  // stored chunk held at this slot
+      if (vt_col(chunk * 8 + (col & 7)) >= valid) dV[e] = (bf16)0.f;
     }
   };
-  auto step = [&](int p, bf16x8 (&fk)[NCH], bf16x8 (&fv)[NCH], const bf16x8 (&nk)[NCH], const bf16x8 (&nv)[NCH]) {
-    // fk/fv held page p (already in LDS) and now take page p+2; nk/nv hold page p+1
-    const int buf = p & 1;
-    gload(p + 2, fk, fv);
+  const bool partial = kv_len % kPage != 0;
+  dma(0, sK0, sV0);
+  __syncthreads();
+  if (n_pages == 1 && partial) {
+    zero_tail(0, sV0);
+    __syncthreads();
+  }
+  auto step = [&](int p, const bf16* cK, const bf16* cV, bf16* nK, bf16* nV) {
+    if (p + 1 < n_pages) dma(p + 1, nK, nV);
     if (wave_active) {
       const int key0 = p * kPage;
       // masking is needed on the request's last (partial) page and, when
@@ -259,19 +280,17 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
         }
         return ok ? x : -INFINITY;
       };
-      mfma_attend_tile<DH, KLD, VLD>(sK[buf], sV[buf], qf, acc, scale_log2, l32, hi, needs_mask, mask);
+      mfma_attend_tile<DH, KLD, VLD, decltype(mask), true>(cK, cV, qf, acc, scale_log2, l32, hi, needs_mask, mask);
     }
-    if (p + 1 < n_pages) lstore(buf ^ 1, p + 1, nk, nv);
-    __syncthreads();
+    __syncthreads();  // page p+1 in LDS for every wave; page p no longer read
+    if (p + 2 == n_pages && partial) {
+      zero_tail(p + 1, nV);
+      __syncthreads();
+    }
   };
-
-  gload(0, ka, va);
-  gload(1, kb, vb);
-  lstore(0, 0, ka, va);
-  __syncthreads();
   for (int p = 0; p < n_pages; p += 2) {
-    step(p, ka, va, kb, vb);
-    if (p + 1 < n_pages) step(p + 1, kb, vb, ka, va);
+    step(p, sK0, sV0, sK1, sV1);
+    if (p + 1 < n_pages) step(p + 1, sK1, sV1, sK0, sV0);
   }
   if (q_valid) mfma_store_out<DH>(acc, out + (size_t)row * ldo + h * DH, hi);
 }
