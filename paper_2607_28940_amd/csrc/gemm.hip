@@ -7,13 +7,18 @@
 //
 // bf16 path: v_mfma_f32_32x32x16_bf16 with fp32 accumulation. The weight tile
 // is the MFMA "A" operand and the activation tile the "B" operand, so each
-// lane's accumulator holds 4 consecutive output columns of one row. Operand
-// tiles are staged global -> registers -> LDS (rows padded by 16 bytes, no bank
-// conflicts), double-buffered, prefetched one K step ahead. Blocks are
-// renumbered so that each of the 8 XCDs (the hardware deals workgroup b to XCD
-// b % 8) works through a contiguous range of tiles, walked in groups of row
-// blocks so that operand blocks are reused from that XCD's L2.
+// lane's accumulator holds 4 consecutive output columns of one row. Large
+// products run on a persistent kernel (one block per CU walking 256x256 tiles,
+// see gemm_bf16_p4); the others on one block per tile with operands staged
+// global -> registers -> LDS (rows padded by 16 bytes, no bank conflicts),
+// double-buffered, prefetched one K step ahead. Tiles are numbered so that each
+// of the 8 XCDs (the hardware deals workgroup b to XCD b % 8) works through a
+// contiguous range of them, walked in groups of row blocks so that operand
+// blocks are reused from that XCD's L2.
 #include "tx_internal.h"
+
+#include <algorithm>
+#include <type_traits>
 
 namespace tx {
 
@@ -288,6 +293,268 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_mfma_256(const bf16* __restr
   }
 }
 
+// Persistent four-wave kernel: one block per CU walks a run of 256x256 output
+// tiles. Four waves (one per SIMD) as 2x2, each wave 128x128 of C from 4x4
+// v_mfma_f32_32x32x16_bf16 tiles with the fp32 accumulators in AGPRs, so every
+// 1 KB fragment read from LDS feeds four MFMAs. K advances 64 at a time through
+// two LDS stages (A and B tiles of 128-byte rows; 16-byte slot s of row r is
+// held at slot s ^ ((r / 2) % 8), so row-wise stores and column-wise fragment
+// reads are both free of bank conflicts without padding).
+//
+// Operands travel global -> registers -> LDS in four groups of 64 bytes per
+// thread. Group q >= 1 of k step t + 1 is parked during sub-step q - 1 of step t
+// and group 0 of step t + 2 during its sub-step 3 (right after the barrier that
+// frees the stage), each group being refetched as soon as it is parked: every
+// load has one whole k step of MFMA work to land, and the loads are spread
+// evenly over the step instead of arriving in one burst. The load stream runs
+// across tile boundaries and the epilogue parks results in an LDS area of its
+// own, so the pipeline never drains between tiles.
+constexpr int PT = 256, PK = 64, kPStage = 2 * PT * PK;
+
+#define TX_LGKM_BARRIER() asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory")
+
+template <int EPI>
+__global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ A, int lda,
+                                                       const bf16* __restrict__ Bt,
+                                                       const float* __restrict__ bias,
+                                                       const bf16* __restrict__ R, int ldr, bf16* __restrict__ C,
+                                                       int ldc, int M, int N, int K, int tiles_m, int tiles_n,
+                                                       int n_tiles, int per_xcd) {
+  __shared__ __attribute__((aligned(16))) bf16 lds[2 * kPStage];
+  __shared__ __attribute__((aligned(16))) float park_all[4 * 32 * 64];
+
+  const int nloc = gridDim.x >> 3, local = blockIdx.x >> 3;
+  const int t_begin = (blockIdx.x & 7) * per_xcd, t_end = min(n_tiles, t_begin + per_xcd);
+  const int my_tiles = t_begin + local < t_end ? (t_end - t_begin - local + nloc - 1) / nloc : 0;
+  if (my_tiles == 0) return;
+  const int nk = K / PK;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l32 = lane & 31, hi = lane >> 5;
+
+  auto tile_origin = [&](int i, int& m0, int& n0) {
+    const int t = t_begin + local + min(i, my_tiles - 1) * nloc;
+    const int group = t / (kGroupM * tiles_n);
+    const int first_m = group * kGroupM;
+    const int gm_size = min(tiles_m - first_m, kGroupM);
+    m0 = (first_m + (t % (kGroupM * tiles_n)) % gm_size) * PT;
+    n0 = ((t % (kGroupM * tiles_n)) / gm_size) * PT;
+  };
+
+  // staging: chunk u of this thread is row (tid / 8) + 32 u, 16-byte slot
+  // tid % 8 of both operand tiles; group q holds chunks 2q and 2q + 1
+  const int srow = tid >> 3, sslot = tid & 7;
+  const int wofs = srow * PK + ((sslot ^ ((srow >> 1) & 7)) << 3);
+  bf16x8 ga[8], gb[8];
+  // rows past M read row M - 1 (their results are never distinct from it)
+  auto gload = [&](auto Q_, int m0, int n0, int k0) {
+    constexpr int Q = decltype(Q_)::value;
+    const int mlim = M - 1 - m0;
+#pragma unroll
+    for (int v = 0; v < 2; ++v) {
+      const int u = 2 * Q + v;
+      ga[u] = *reinterpret_cast<const bf16x8*>(A + (m0 + min(srow + 32 * u, mlim)) * lda + sslot * 8 + k0);
+      gb[u] = *reinterpret_cast<const bf16x8*>(Bt + (n0 + srow + 32 * u) * K + sslot * 8 + k0);
+    }
+  };
+  auto lstore = [&](auto Q_, int stage) {
+    constexpr int Q = decltype(Q_)::value;
+    bf16* sa = lds + stage * kPStage;
+#pragma unroll
+    for (int v = 0; v < 2; ++v) {
+      const int u = 2 * Q + v;
+      *reinterpret_cast<bf16x8*>(sa + wofs + u * 32 * PK) = ga[u];
+      *reinterpret_cast<bf16x8*>(sa + PT * PK + wofs + u * 32 * PK) = gb[u];
+    }
+  };
+
+  // fragment reads: A rows wm*128 + 32 j + l32, B rows wn*128 + 32 i + l32;
+  // k sub-step ks covers slots 2 ks + hi
+  int rofs[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) rofs[ks] = l32 * PK + (((2 * ks + hi) ^ ((l32 >> 1) & 7)) << 3);
+  const int a_base = wm * 128 * PK, b_base = PT * PK + wn * 128 * PK;
+  auto fread = [&](bf16x8(&fa)[4], bf16x8(&fb)[4], int stage, int ks) {
+    const bf16* s = lds + stage * kPStage;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      fa[q] = *reinterpret_cast<const bf16x8*>(s + a_base + q * 32 * PK + rofs[ks]);
+      fb[q] = *reinterpret_cast<const bf16x8*>(s + b_base + q * 32 * PK + rofs[ks]);
+    }
+  };
+
+  floatx16 acc[4][4];
+  bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
+  auto mfma16 = [&](const bf16x8(&fa)[4], const bf16x8(&fb)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[i], fa[j], acc[i][j], 0, 0, 0);
+  };
+  // 16 MFMAs with 8 fragment reads, 4 LDS stores and 4 global loads between them
+  auto interleave = [&]() {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+
+  // tile-local k step -> (tile origin, column): steps past the tile belong to
+  // the next one (the last tile stands in for a next tile that does not exist)
+  int m0, n0, nm0, nn0;
+  auto target = [&](int kt, int& tm0, int& tn0, int& k0) {
+    const bool nxt = kt >= nk;
+    tm0 = nxt ? nm0 : m0;
+    tn0 = nxt ? nn0 : n0;
+    k0 = (nxt ? kt - nk : kt) * PK;
+  };
+
+  // One k step on stage S (= kt % 2); see the kernel comment for the order
+  auto step = [&](auto S_, int kt) {
+    constexpr int S = decltype(S_)::value;
+    int am0, an0, ak0, bm0, bn0, bk0;
+    target(kt + 2, am0, an0, ak0);
+    target(kt + 3, bm0, bn0, bk0);
+    fread(fa1, fb1, S, 1);
+    lstore(I1{}, S ^ 1);
+    gload(I1{}, am0, an0, ak0);
+    mfma16(fa0, fb0);
+    interleave();
+    fread(fa0, fb0, S, 2);
+    lstore(I2{}, S ^ 1);
+    gload(I2{}, am0, an0, ak0);
+    mfma16(fa1, fb1);
+    interleave();
+    fread(fa1, fb1, S, 3);
+    lstore(I3{}, S ^ 1);
+    gload(I3{}, am0, an0, ak0);
+    mfma16(fa0, fb0);
+    interleave();
+    TX_LGKM_BARRIER();
+    fread(fa0, fb0, S ^ 1, 0);
+    lstore(I0{}, S);
+    gload(I0{}, bm0, bn0, bk0);
+    mfma16(fa1, fb1);
+    interleave();
+  };
+
+  // prologue: stage 0 = step 0, group 0 of step 1 in stage 1; registers hold
+  // group 0 of step 2 and groups 1..3 of step 1
+  tile_origin(0, m0, n0);
+  tile_origin(1, nm0, nn0);
+  {
+    int tm0, tn0, k0;
+    gload(I0{}, m0, n0, 0);
+    gload(I1{}, m0, n0, 0);
+    gload(I2{}, m0, n0, 0);
+    gload(I3{}, m0, n0, 0);
+    lstore(I0{}, 0);
+    lstore(I1{}, 0);
+    lstore(I2{}, 0);
+    lstore(I3{}, 0);
+    target(1, tm0, tn0, k0);
+    gload(I0{}, tm0, tn0, k0);
+    lstore(I0{}, 1);
+    gload(I1{}, tm0, tn0, k0);
+    gload(I2{}, tm0, tn0, k0);
+    gload(I3{}, tm0, tn0, k0);
+    target(2, tm0, tn0, k0);
+    gload(I0{}, tm0, tn0, k0);
+  }
+  TX_LGKM_BARRIER();
+  fread(fa0, fb0, 0, 0);
+
+  float* park = park_all + wave * 32 * 64;
+  const int er = lane >> 3, ec = lane & 7;  // row (plus 8 u) and 8-float chunk of the read-back
+
+  for (int i = 0; i < my_tiles; ++i) {
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
+    for (int kt = 0; kt < nk; kt += 2) {
+      step(I0{}, kt);
+      step(I1{}, kt + 1);
+    }
+    const int cm0 = m0, cn0 = n0;
+    m0 = nm0;
+    n0 = nn0;
+    tile_origin(i + 2, nm0, nn0);
+
+    // epilogue: per round each wave parks 32 rows x 64 columns of fp32 results
+    // (16-byte unit q of row r at unit q ^ (r % 16): conflict-free both ways)
+    // and reads them back row-contiguously, 8 lanes per 128-byte row segment;
+    // bias, GELU or residual applied with one rounding to bf16. Rows past M
+    // rewrite row M - 1 with its own values.
+    floatx4 bv[2][2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      bv[h][0] = *reinterpret_cast<const floatx4*>(bias + cn0 + wn * 128 + 64 * h + ec * 8);
+      bv[h][1] = *reinterpret_cast<const floatx4*>(bias + cn0 + wn * 128 + 64 * h + ec * 8 + 4);
+    }
+    bf16x8 rres[4];
+    auto rload = [&](int j, int h) {
+      if (EPI == EPI_BIAS_RESID) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int m = min(cm0 + wm * 128 + j * 32 + er + 8 * u, M - 1);
+          rres[u] = *reinterpret_cast<const bf16x8*>(R + (size_t)m * ldr + cn0 + wn * 128 + 64 * h + ec * 8);
+        }
+      }
+    };
+    rload(0, 0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const floatx4 v4 = {acc[2 * h + ii][j][4 * g], acc[2 * h + ii][j][4 * g + 1], acc[2 * h + ii][j][4 * g + 2],
+                                acc[2 * h + ii][j][4 * g + 3]};
+            const int q = ii * 8 + 2 * g + hi;
+            *reinterpret_cast<floatx4*>(park + l32 * 64 + ((q ^ (l32 & 15)) << 2)) = v4;
+          }
+        bf16x8 rcur[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) rcur[u] = rres[u];
+        if (j * 2 + h + 1 < 8) rload((j * 2 + h + 1) >> 1, (j * 2 + h + 1) & 1);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int r = er + 8 * u;
+          const floatx4 x0 = *reinterpret_cast<const floatx4*>(park + r * 64 + (((2 * ec) ^ (r & 15)) << 2));
+          const floatx4 x1 = *reinterpret_cast<const floatx4*>(park + r * 64 + (((2 * ec + 1) ^ (r & 15)) << 2));
+          const int m = min(cm0 + wm * 128 + j * 32 + r, M - 1);
+          bf16x8 o;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float r0 = EPI == EPI_BIAS_RESID ? (float)rcur[u][e] : 0.f;
+            const float r1 = EPI == EPI_BIAS_RESID ? (float)rcur[u][e + 4] : 0.f;
+            o[e] = (bf16)epilogue<EPI>(x0[e], bv[h][0][e], r0);
+            o[e + 4] = (bf16)epilogue<EPI>(x1[e], bv[h][1][e], r1);
+          }
+          *reinterpret_cast<bf16x8*>(C + (size_t)m * ldc + cn0 + wn * 128 + 64 * h + ec * 8) = o;
+        }
+      }
+  }
+}
+
 // Plain tiled GEMM for fp32 models and shapes the MFMA tiling does not cover:
 // 64x64 block tile, K step 16, each thread computes 4x4 outputs in fp32.
 template <typename T, int EPI>
@@ -366,6 +633,35 @@ hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const fl
                        (((uintptr_t)bias & 15) == 0);
   if (N % GN != 0 || K % GK != 0 || !aligned)
     return plain<bf16>(A, lda, Bt, bias, R, ldr, C, ldc, M, N, K, epi, s);
+  // Persistent kernel: K a multiple of 128 and at least 256 (its load stream
+  // runs three k steps ahead), element offsets within int32.
+  if (N % PT == 0 && K % (2 * PK) == 0 && K >= 4 * PK && M >= 2048 && (long long)M * lda < (1ll << 31) &&
+      (long long)N * K < (1ll << 31)) {
+    static int n_cu = 0;
+    if (n_cu <= 0) {
+      int dev = 0;
+      if (hipGetDevice(&dev) != hipSuccess ||
+          hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 8)
+        n_cu = 256;
+    }
+    const int tiles_n = N / PT, tiles_m = (M + PT - 1) / PT, n_tiles = tiles_n * tiles_m;
+    const int per_xcd = (n_tiles + 7) / 8;
+    const int grid = 8 * std::max(1, std::min(n_cu / 8, per_xcd));
+    const bf16* a = (const bf16*)A;
+    const bf16* b = (const bf16*)Bt;
+    const bf16* r = (const bf16*)R;
+    bf16* c = (bf16*)C;
+#define TX_GP4(E)                                                                                             \
+  gemm_bf16_p4<E><<<grid, 256, 0, s>>>(a, lda, b, bias, r, ldr, c, ldc, M, N, K, tiles_m, tiles_n, n_tiles, \
+                                       per_xcd)
+    switch (epi) {
+      case EPI_BIAS: TX_GP4(EPI_BIAS); break;
+      case EPI_BIAS_GELU: TX_GP4(EPI_BIAS_GELU); break;
+      case EPI_BIAS_RESID: TX_GP4(EPI_BIAS_RESID); break;
+    }
+#undef TX_GP4
+    return hipGetLastError();
+  }
   if (N % BN == 0 && M >= 2048) {
     const int tiles_n = N / BN, tiles_m = (M + BM - 1) / BM, n_tiles = tiles_n * tiles_m;
     const int grid = ((n_tiles + 7) / 8) * 8;

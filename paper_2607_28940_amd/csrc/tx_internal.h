@@ -87,7 +87,8 @@ struct PageGeom {
 
 enum Epilogue { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2 };
 
-// C[M][N] (ldc) = epi(A[M][K] (lda) * Bt[N][K]^T + bias[N] (+ R[M][N] (ldr)))
+// C[M][N] (ldc) = epi(A[M][K] (lda) * Bt[N][K]^T + bias[N] (+ R[M][N] (ldr))).
+// C must not overlap A or R (rows of a partial last tile rewrite row M - 1).
 hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const float* bias, const void* R, int ldr,
                        void* C, int ldc, int M, int N, int K, Epilogue epi, hipStream_t s);
 
