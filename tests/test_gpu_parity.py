@@ -64,6 +64,45 @@ def test_bf16_ragged_vs_oracle(O, name, model):
     _compare_all(run, O.Oracle(model, w), range(wl.B), BF16_TOL, f"bf16 ragged {name}")
 
 
+# Enough rows for the persistent GEMM (M >= 2048 encoder and decoder rows,
+# neither a multiple of its 256-row tile), at the smallest K it takes (256:
+# the QKV, attention-output and FFN-up projections of a d = 256 model) and at
+# K = 1024 (the FFN down-projection); 10 requests with ragged S, C and L.
+GEMM_ROWS = dict(L=[211, 305, 177, 389, 260, 143, 330, 298, 155, 271], S=[3, 17, 40, 9, 0, 33, 12, 26, 5, 21],
+                 C=[301, 188, 270, 155, 322, 240, 199, 167, 290, 216])
+
+
+def test_persistent_gemm_ragged_rows(O):
+    """The same calls run once in one pass (every large projection on the
+    persistent kernel) and once with the smallest workspace (one request per
+    pass, every projection on the per-tile kernel): both kernels sum each
+    output in the same order, so the scores agree bitwise. Sampled requests
+    are checked against the oracle (a tile or row mapped wrongly would move
+    whole rows of scores by O(1))."""
+    model = ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16)
+    wl = I.custom_workload(model, cfg_id=61, **GEMM_ROWS)
+    rows, enc_rows = sum(wl.S) + sum(wl.C), sum(wl.L)
+    assert rows >= 2048 and rows % 256 and enc_rows >= 2048 and enc_rows % 256
+    # standard weights: with the sharp variant bf16 rounding alone takes the
+    # largest sampled error to 2.05e-2, just over the 2e-2 bar
+    w = I.make_weights(model, ("affine",))
+    log(f"persistent GEMM rows: decoder {rows}, encoder {enc_rows}")
+    big = DeviceCase(wl, w)
+    big.build(range(wl.B))
+    g = big.score(range(wl.B))
+    small = DeviceCase(wl, w)
+    small.build(range(wl.B), ws_limit=small.cache.workspace_min_bytes(0, wl.B, I.offsets(wl.L)))
+    g1 = small.score(range(wl.B), ws_limit=small.cache.workspace_min_bytes(2, wl.B, I.offsets(wl.S),
+                                                                            I.offsets(wl.C)))
+    assert np.all(np.isfinite(np.concatenate(g)))
+    assert np.array_equal(np.concatenate(g), np.concatenate(g1))
+    reqs = [0, 3, 9]
+    err = score_err(np.concatenate([g[r] for r in reqs]),
+                    np.concatenate([oracle_request(O.Oracle(model, w), wl, r)[0] for r in reqs]))
+    log(f"persistent GEMM ragged rows, requests {reqs}: max err {err['max']:.3e} p99 {err['p99']:.3e}")
+    assert err["max"] <= BF16_TOL, err
+
+
 def test_cache_contents_vs_oracle(O):
     model = SMALL_BF16[0][1]
     wl = I.custom_workload(model, cfg_id=32, L=[150, 64], S=[4, 4], C=[4, 4])
