@@ -6,6 +6,8 @@
 //   the paged cache layout, cache export, and weight repacking.
 #include "tx_internal.h"
 
+#include <algorithm>
+
 namespace tx {
 
 // Decoder head on one wave's row, given this lane's share of the normalised
@@ -48,44 +50,64 @@ __device__ __forceinline__ void head_out(const float (&z)[CNT], int c0, int stri
   if (lane < n_act) scores[(size_t)row * n_act + lane] = e / den;
 }
 
-// One wave per row; EPL features per lane held in registers (EPL = d / 64).
-// Two-pass mean / variance in fp32 from the register copy.
+// One wave per row at a time; EPL features per lane held in registers
+// (EPL = d / 64). Each wave walks rows wave_id, wave_id + n_waves, ... so the
+// gain and bias it needs are loaded once, and the next row's features are
+// requested before the current row is normalised. Two-pass mean / variance
+// in fp32 from the register copy.
 template <typename T, int EPL, bool SCORE>
 __global__ __launch_bounds__(256) void layernorm_rows(const T* __restrict__ x, T* __restrict__ y,
                                                       const float* __restrict__ g, const float* __restrict__ b,
                                                       const float* __restrict__ w, const float* __restrict__ b0,
                                                       float* __restrict__ scores, int M, int d, float eps, int n_act) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int lane = threadIdx.x & 63;
+  const int n_waves = gridDim.x * 4;
+  int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
-  const T* xr = x + (size_t)row * d + lane * EPL;
-  float v[EPL];
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) v[e] = (float)xr[e];
-  float sum = 0.f;
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) sum += v[e];
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
-  const float mean = sum / d;
-  float sq = 0.f;
+  const int c0 = lane * EPL;
+  float gv[EPL], bv[EPL];
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
-    const float t = v[e] - mean;
-    sq += t * t;
+    gv[e] = g[c0 + e];
+    bv[e] = b[c0 + e];
   }
+  T nx[EPL];
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) sq += __shfl_xor(sq, o);
-  const float inv = rsqrtf(sq / d + eps);
-  const int c0 = lane * EPL;
-  if (SCORE) {
-    float z[EPL];
+  for (int e = 0; e < EPL; ++e) nx[e] = x[(size_t)row * d + c0 + e];
+  for (; row < M; row += n_waves) {
+    float v[EPL];
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) z[e] = (v[e] - mean) * inv * g[c0 + e] + b[c0 + e];
-    head_out<EPL>(z, c0, 1, EPL, lane, d, w, b0, scores, row, n_act);
-  } else {
-    T* yr = y + (size_t)row * d + c0;
+    for (int e = 0; e < EPL; ++e) v[e] = (float)nx[e];
+    const int next = row + n_waves;
+    if (next < M) {
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) yr[e] = (T)((v[e] - mean) * inv * g[c0 + e] + b[c0 + e]);
+      for (int e = 0; e < EPL; ++e) nx[e] = x[(size_t)next * d + c0 + e];
+    }
+    float sum = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) sum += v[e];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+    const float mean = sum / d;
+    float sq = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      const float t = v[e] - mean;
+      sq += t * t;
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) sq += __shfl_xor(sq, o);
+    const float inv = rsqrtf(sq / d + eps);
+    if (SCORE) {
+      float z[EPL];
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) z[e] = (v[e] - mean) * inv * gv[e] + bv[e];
+      head_out<EPL>(z, c0, 1, EPL, lane, d, w, b0, scores, row, n_act);
+    } else {
+      T* yr = y + (size_t)row * d + c0;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) yr[e] = (T)((v[e] - mean) * inv * gv[e] + bv[e]);
+    }
   }
 }
 
@@ -131,9 +153,11 @@ static hipError_t ln_dispatch(const void* x, void* y, const float* g, const floa
                               float* scores, int M, int d, float eps, int n_act, hipStream_t s) {
   if (M <= 0) return hipSuccess;
   const int blocks = (M + 3) / 4;
+  // register-resident widths: at most 8 rows per wave (2048 blocks of 4 waves)
+  const int rblocks = std::min(blocks, std::max(2048, (blocks + 7) / 8));
   const T* xx = (const T*)x;
   T* yy = (T*)y;
-#define TX_LN(E) layernorm_rows<T, E, SCORE><<<blocks, 256, 0, s>>>(xx, yy, g, b, w, b0, scores, M, d, eps, n_act)
+#define TX_LN(E) layernorm_rows<T, E, SCORE><<<rblocks, 256, 0, s>>>(xx, yy, g, b, w, b0, scores, M, d, eps, n_act)
   switch (d) {
     case 64: TX_LN(1); break;
     case 128: TX_LN(2); break;
