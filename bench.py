@@ -133,7 +133,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="headline", choices=["headline", "uniform", "ragged", "tiny"])
+    ap.add_argument("--workload", default="headline", choices=["headline", "uniform", "ragged", "tiny", "append"])
     ap.add_argument("--l-local", type=int, default=0,
                     help="local-global sparse cross-attention window (0: dense cross-attention, the headline)")
     ap.add_argument("--no-global-token", action="store_true",
@@ -144,6 +144,9 @@ def main():
                     help="k >= 2: softmax decoder head over k action tokens (0: the scalar logit head)")
     ap.add_argument("--cpu-requests", type=int, default=None,
                     help="requests in the oracle's timed sample (default: about 10 s of CPU work)")
+    ap.add_argument("--append", action="store_true",
+                    help="workload 'append': each timed step first appends the workload's n_append events to "
+                         "every user's cache (through the causal encoder, in place), then scores")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-launch events")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
@@ -177,8 +180,12 @@ def main():
     # caches of the users (every request, or B/T users with T events each)
     n_users = max(1, wl.B // args.events) if args.events else wl.B
     users = list(range(n_users))
-    n_pages = sum((wl.L[u] + 63) // 64 for u in users)
-    cache = T.KVCache(model, n_pages=n_pages, max_requests=n_users, max_tokens=max(wl.L))
+    if args.append and (wl.n_append <= 0 or args.events):
+        print("--append needs a workload with appended events (--workload append) and no --events", file=sys.stderr)
+        sys.exit(2)
+    grow = wl.n_append * (args.warmup + args.steps) if args.append else 0  # tokens appended per user
+    n_pages = sum((wl.L[u] + grow + 63) // 64 for u in users)
+    cache = T.KVCache(model, n_pages=n_pages, max_requests=n_users, max_tokens=max(wl.L) + grow)
     # build every user's cache (untimed), a few at a time
     chunk = max(1, (1 << 19) // max(1, max(wl.L)))
     for a in range(0, n_users, chunk):
@@ -198,7 +205,13 @@ def main():
         prefix = [max(1, wl.L[ids[e]] * (e % args.events + 1) // args.events) for e in range(wl.B)]
         wl = dataclasses.replace(wl, L=prefix)
 
+    if args.append:
+        xe = T.to_device(I.packed_tokens(wl, I.STREAM_EVENTS, users, threads=16), m)
+        eo = I.offsets([wl.n_append] * n_users)
+
     def step():
+        if args.append:
+            cache.append(users, xe, eo, ws_limit=8 << 30)
         if prefix is None:
             cache.score(ids, xs, so, xc, co, out=out)
         else:
@@ -234,7 +247,11 @@ def main():
         T.profile_enable(False)
     assert bool(torch.isfinite(out).all()), "non-finite scores"
 
-    work = score_work(wl)
+    if args.append:  # cached length grows by n_append per step; the work model takes the timed average
+        avg_len = [L + wl.n_append * (args.warmup + (args.steps + 1) / 2) for L in wl.L]
+        work = score_work(dataclasses.replace(wl, L=[int(round(x)) for x in avg_len]))
+    else:
+        work = score_work(wl)
     n_scores = int(co[-1])
     value = n_scores / (ms / 1e3)
     tflops = work["flop"] / (ms / 1e3) / 1e12
@@ -278,7 +295,18 @@ def main():
     else:
         mode = "dense cross-attention over every cached token"
     head = f"softmax over {m.n_actions} action tokens" if m.n_actions else "scalar logit head"
-    if args.events:
+    append_info = None
+    if args.append:
+        enc = {k: v for k, v in prof.items() if k.startswith("encode.")}
+        app_ms = sum(v["ms"] for v in enc.values()) / args.steps if enc else None
+        append_info = {"events_per_step": wl.n_append * n_users,
+                       "append_ms_per_step": round(app_ms, 4) if app_ms is not None else None,
+                       "events_per_s": round(wl.n_append * n_users / (app_ms / 1e3), 1) if app_ms else None}
+    if args.append:
+        metric = (f"candidate scores/sec with incremental append: {n_users} users, {wl.n_append} events appended "
+                  f"per user (causal encoder against the cached prefix, in place) then scored, {mode}, "
+                  f"{head} on 1 MI355X")
+    elif args.events:
         metric = (f"candidate scores/sec, event-sliced decoding (seq2seq training forward): {n_users} users x "
                   f"{args.events} serving events of the {args.workload} shape, each against its own cache prefix, "
                   f"with {mode} and {head} on 1 MI355X")
@@ -298,7 +326,8 @@ def main():
                    "global_batch": wl.B, "scores_per_step": n_scores, "cross_attention": mode,
                    "head": head,
                    "events": ({"users": n_users, "per_user": args.events,
-                               "prefixes": "L (t + 1) / T"} if args.events else None)},
+                               "prefixes": "L (t + 1) / T"} if args.events else None),
+                   "append": append_info},
         "mfma_frac_of_peak": round(tflops / peak, 4),
         "achieved_tflops": round(tflops, 2),
         "algorithmic": {"flop_per_step": work["flop"], "bytes_per_step": work["bytes"]},
