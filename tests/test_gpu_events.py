@@ -12,7 +12,7 @@ import pytest
 from paper_2607_28940_amd import inputs as I
 from paper_2607_28940_amd import transx as T
 from paper_2607_28940_amd.inputs import ModelConfig
-from tests.parity_util import BF16_TOL, FP32_TOL, DeviceCase, log, score_err
+from tests.parity_util import BF16_TOL, FP32_TOL, DeviceCase, check_err, log, score_err
 
 pytestmark = pytest.mark.gpu
 
@@ -82,7 +82,7 @@ def test_events_vs_oracle(oracle_mod, name, model, variant, tol):
     assert np.all(np.isfinite(G))
     err = score_err(G, O)
     log(f"events {name}: max err {err['max']:.3e} p99 {err['p99']:.3e} (tol {tol})")
-    assert err["max"] <= tol, err
+    check_err(err, tol)
 
 
 def test_full_prefix_events_equal_score_candidates():

@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 from paper_2607_28940_amd import inputs as I
-from tests.parity_util import BF16_TOL, DeviceCase, log, oracle_request, score_err, tensor_err
+from tests.parity_util import BF16_TOL, DeviceCase, check_err, log, oracle_request, score_err, tensor_err
 
 pytestmark = pytest.mark.gpu
 
@@ -32,7 +32,7 @@ def _check_sampled(run, orc, reqs, label):
     want = np.concatenate([oracle_request(orc, run.wl, r)[0] for r in reqs])
     err = score_err(got, want)
     log(f"{label}: sampled requests {list(reqs)}: max err {err['max']:.3e} p99 {err['p99']:.3e}")
-    assert err["max"] <= BF16_TOL, err
+    check_err(err, BF16_TOL)
     return g
 
 
@@ -130,7 +130,7 @@ def test_append_full(oracle_mod):
     o = oracle_request(orc, wl, 0, append=True)[0]
     err = score_err(g[0], o)
     log(f"append: user 0 vs oracle on the re-encoded sequence: max err {err['max']:.3e} p99 {err['p99']:.3e}")
-    assert err["max"] <= BF16_TOL, err
+    check_err(err, BF16_TOL)
     # the last user's appended cache equals a rebuild of all its tokens
     last = wl.B - 1
     appended = [run.cache.export(last, p, l).float().cpu().numpy() for p in range(4) for l in range(2)]

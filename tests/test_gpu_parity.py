@@ -6,7 +6,7 @@ import pytest
 
 from paper_2607_28940_amd import inputs as I
 from paper_2607_28940_amd.inputs import ModelConfig
-from tests.parity_util import BF16_TOL, FP32_TOL, DeviceCase, log, oracle_request, score_err, tensor_err
+from tests.parity_util import BF16_TOL, FP32_TOL, DeviceCase, check_err, log, oracle_request, score_err, tensor_err
 
 pytestmark = pytest.mark.gpu
 
@@ -29,7 +29,7 @@ def _compare_all(run: DeviceCase, orc, reqs, tol, label, append=False):
     err = score_err(np.concatenate(g), np.concatenate(o))
     log(f"{label}: max err {err['max']:.3e} p99 {err['p99']:.3e} (tol {tol})")
     assert np.all(np.isfinite(np.concatenate(g)))
-    assert err["max"] <= tol, err
+    check_err(err, tol)
     return g, o
 
 
@@ -100,7 +100,7 @@ def test_persistent_gemm_ragged_rows(O):
     err = score_err(np.concatenate([g[r] for r in reqs]),
                     np.concatenate([oracle_request(O.Oracle(model, w), wl, r)[0] for r in reqs]))
     log(f"persistent GEMM ragged rows, requests {reqs}: max err {err['max']:.3e} p99 {err['p99']:.3e}")
-    assert err["max"] <= BF16_TOL, err
+    check_err(err, BF16_TOL)
 
 
 def test_cache_contents_vs_oracle(O):
@@ -150,7 +150,7 @@ def test_append_equals_rebuild(O):
     o = np.concatenate([oracle_request(orc, wl, r, append=True)[0] for r in (0, 1)])
     err = score_err(g_inc, o)
     log(f"append scores vs oracle: {err}")
-    assert err["max"] <= BF16_TOL
+    check_err(err, BF16_TOL)
 
 
 def test_candidates_independent_on_gpu():

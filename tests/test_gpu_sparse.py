@@ -14,7 +14,7 @@ import pytest
 
 from paper_2607_28940_amd import inputs as I
 from paper_2607_28940_amd.inputs import ModelConfig
-from tests.parity_util import BF16_TOL, FP32_TOL, DeviceCase, log, oracle_request, score_err, tensor_err
+from tests.parity_util import BF16_TOL, FP32_TOL, DeviceCase, check_err, log, oracle_request, score_err, tensor_err
 
 pytestmark = pytest.mark.gpu
 
@@ -36,7 +36,7 @@ def _compare(run, orc, reqs, tol, label, append=False):
     err = score_err(g, o)
     log(f"{label}: max err {err['max']:.3e} p99 {err['p99']:.3e} (tol {tol})")
     assert np.all(np.isfinite(g))
-    assert err["max"] <= tol, err
+    check_err(err, tol)
     return g, o
 
 
@@ -132,4 +132,4 @@ def test_sparse_append_folds_pooling_state(oracle_mod):
     o = np.concatenate([oracle_request(orc, wl, r, append=True)[0] for r in (0, 1, 2)])
     err = score_err(g_inc, o)
     log(f"sparse append scores vs oracle: {err}")
-    assert err["max"] <= BF16_TOL
+    check_err(err, BF16_TOL)
