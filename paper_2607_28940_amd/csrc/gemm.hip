@@ -22,27 +22,31 @@
 
 namespace tx {
 
-// GELU(x) = x * Phi(x) = 0.5 x erfc(-x / sqrt 2), with erfc from the Chebyshev
-// fit of Press et al. (Numerical Recipes, erfcc; fractional error below 1.2e-7
-// for every argument, so the negative tail keeps its relative accuracy):
-//   erfc(z) = t exp(-z^2 + P(t)),  t = 1 / (1 + z/2),  z >= 0.
-// One reciprocal, one exp2 and 9 FMAs instead of the library erff.
+// GELU(x) = x Phi(x). With u = |x|, Phi(-u) = erfc(u / sqrt 2) / 2 comes from
+// the Chebyshev fit of Press et al. (Numerical Recipes, erfcc; fractional
+// error below 1.2e-7 for every argument, so the negative tail keeps its
+// relative accuracy):
+//   erfc(z) = t exp(-z^2 + P(t)),  t = 1 / (1 + z/2),  z = u / sqrt 2,
+// evaluated as Phi(-u) = t 2^(P'(t) - (c u)^2) with P' = log2(e) P - 1 and
+// c^2 = log2(e) / 2 (change of base and the halving folded into the
+// coefficients). Then x Phi(x) = max(x, 0) - u Phi(-u) for either sign of x:
+// one reciprocal, one exp2 and 12 FMA-type operations.
 __device__ __forceinline__ float gelu_erf(float x) {
-  const float z = fabsf(x) * 0.70710678118654752f;
-  const float t = __builtin_amdgcn_rcpf(1.0f + 0.5f * z);
-  float p = 0.17087277f;
-  p = fmaf(p, t, -0.82215223f);
-  p = fmaf(p, t, 1.48851587f);
-  p = fmaf(p, t, -1.13520398f);
-  p = fmaf(p, t, 0.27886807f);
-  p = fmaf(p, t, -0.18628806f);
-  p = fmaf(p, t, 0.09678418f);
-  p = fmaf(p, t, 0.37409196f);
-  p = fmaf(p, t, 1.00002368f);
-  p = fmaf(p, t, -1.26551223f);
-  const float e = t * __builtin_amdgcn_exp2f((p - z * z) * 1.4426950408889634f);  // erfc(|x| / sqrt 2)
-  const float h = 0.5f * x * e;
-  return x >= 0.f ? x - h : h;
+  const float u = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(fmaf(u, 0.35355339059327373f, 1.0f));
+  float p = 0.24651729790196045f;
+  p = fmaf(p, t, -1.1861149450768025f);
+  p = fmaf(p, t, 2.147474463933521f);
+  p = fmaf(p, t, -1.637753152343414f);
+  p = fmaf(p, t, 0.40232158165127635f);
+  p = fmaf(p, t, -0.2687568603388257f);
+  p = fmaf(p, t, 0.1396300565225048f);
+  p = fmaf(p, t, 0.5397006155284324f);
+  p = fmaf(p, t, 1.4427292039075317f);
+  p = fmaf(p, t, -2.825748218405333f);
+  const float w = u * 0.8493218002880191f;
+  const float q = t * __builtin_amdgcn_exp2f(fmaf(-w, w, p));  // Phi(-u)
+  return fmaf(-u, q, fmaxf(x, 0.f));
 }
 
 template <int EPI>
@@ -386,12 +390,16 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
 
   floatx16 acc[4][4];
   bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
-  auto mfma16 = [&](const bf16x8(&fa)[4], const bf16x8(&fb)[4]) {
+  auto mfma16 = [&](auto Z_, const bf16x8(&fa)[4], const bf16x8(&fb)[4]) {
+    constexpr bool Z = decltype(Z_)::value;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[i], fa[j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[i], fa[j], Z ? floatx16{} : acc[i][j], 0, 0, 0);
   };
+  using F0 = std::false_type;
+  using T1 = std::true_type;
   // 16 MFMAs with 8 fragment reads, 4 LDS stores and 4 global loads between them
   auto interleave = [&]() {
 #pragma unroll
@@ -423,7 +431,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
   };
 
   // One k step on stage S (= kt % 2); see the kernel comment for the order
-  auto step = [&](auto S_, int kt) {
+  auto step = [&](auto S_, auto Z_, int kt) {
     constexpr int S = decltype(S_)::value;
     int am0, an0, ak0, bm0, bn0, bk0;
     target(kt + 2, am0, an0, ak0);
@@ -431,23 +439,23 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
     fread(fa1, fb1, S, 1);
     lstore(I1{}, S ^ 1);
     gload(I1{}, am0, an0, ak0);
-    mfma16(fa0, fb0);
+    mfma16(Z_, fa0, fb0);
     interleave();
     fread(fa0, fb0, S, 2);
     lstore(I2{}, S ^ 1);
     gload(I2{}, am0, an0, ak0);
-    mfma16(fa1, fb1);
+    mfma16(F0{}, fa1, fb1);
     interleave();
     fread(fa1, fb1, S, 3);
     lstore(I3{}, S ^ 1);
     gload(I3{}, am0, an0, ak0);
-    mfma16(fa0, fb0);
+    mfma16(F0{}, fa0, fb0);
     interleave();
     TX_LGKM_BARRIER();
     fread(fa0, fb0, S ^ 1, 0);
     lstore(I0{}, S);
     gload(I0{}, bm0, bn0, bk0);
-    mfma16(fa1, fb1);
+    mfma16(F0{}, fa1, fb1);
     interleave();
   };
 
@@ -481,15 +489,12 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
   const int er = lane >> 3, ec = lane & 7;  // row (plus 8 u) and 8-float chunk of the read-back
 
   for (int i = 0; i < my_tiles; ++i) {
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int b = 0; b < 4; ++b)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
-    for (int kt = 0; kt < nk; kt += 2) {
-      step(I0{}, kt);
-      step(I1{}, kt + 1);
+    // the tile's first MFMAs take a zero accumulator input
+    step(I0{}, T1{}, 0);
+    step(I1{}, F0{}, 1);
+    for (int kt = 2; kt < nk; kt += 2) {
+      step(I0{}, F0{}, kt);
+      step(I1{}, F0{}, kt + 1);
     }
     const int cm0 = m0, cn0 = n0;
     m0 = nm0;
