@@ -141,9 +141,20 @@ __device__ __forceinline__ void mfma_attend_tile(const bf16* __restrict__ sK, co
   }
 }
 
-// Normalised output of a wave's queries: O[query l32][features] as bf16.
+// Normalises the wave's 32 output rows, parks them in LDS (stage: 32 x DH
+// elements of free LDS for this wave) and stores them row-contiguously, DH / 8
+// lanes per row, instead of 8-byte pieces of 32 rows per store. 16-byte unit u
+// of row r sits at u ^ swz(r): conflict-free for the 8-byte writes and the
+// 16-byte reads. The wave's query r (r < nq) is query q0 + r of its request,
+// whose output row is row_a + q for q < split and row_b + (q - split) after.
 template <int DH>
-__device__ __forceinline__ void mfma_store_out(const MfmaAcc<DH>& acc, bf16* __restrict__ orow, int hi) {
+__device__ __forceinline__ void mfma_store_out_staged(const MfmaAcc<DH>& acc, bf16* __restrict__ stage,
+                                                      bf16* __restrict__ out, int ldo, int col0, int lane, int q0,
+                                                      int nq, int split, int row_a, int row_b) {
+  constexpr int UPR = DH / 8;    // 16-byte units per row
+  constexpr int RPI = 64 / UPR;  // rows per read
+  auto swz = [](int r) { return UPR == 16 ? (r & 15) : ((r >> 1) & 7); };
+  const int l32 = lane & 31, hi = lane >> 5;
   const float inv = acc.l > 0.f ? 1.f / acc.l : 0.f;
 #pragma unroll
   for (int db = 0; db < DH / 32; ++db)
@@ -152,8 +163,18 @@ __device__ __forceinline__ void mfma_store_out(const MfmaAcc<DH>& acc, bf16* __r
       bf16x4 w;
 #pragma unroll
       for (int t = 0; t < 4; ++t) w[t] = (bf16)(acc.o[db][4 * gq + t] * inv);
-      *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * gq + 4 * hi) = w;
+      *reinterpret_cast<bf16x4*>(stage + l32 * DH + (((4 * db + gq) ^ swz(l32)) << 3) + 4 * hi) = w;
     }
+#pragma unroll
+  for (int k = 0; k < 32 / RPI; ++k) {
+    const int r = k * RPI + lane / UPR, q = lane % UPR;
+    const bf16x8 v = *reinterpret_cast<const bf16x8*>(stage + r * DH + ((q ^ swz(r)) << 3));
+    if (r < nq) {
+      const int qq = q0 + r;
+      const int o = qq < split ? row_a + qq : row_b + (qq - split);
+      *reinterpret_cast<bf16x8*>(out + (size_t)o * ldo + col0 + q * 8) = v;
+    }
+  }
 }
 
 // ============================================================================
@@ -199,7 +220,6 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
 
   const int qi = wave * 32 + l32;
   const bool wave_active = wave * 32 < tile.q_count;
-  const bool q_valid = qi < tile.q_count;
   const int i = tile.q_begin + min(qi, tile.q_count - 1);
   const int row = i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
   const int qpos = rq.pos0 + i;
@@ -292,7 +312,10 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
     step(p, sK0, sV0, sK1, sV1);
     if (p + 1 < n_pages) step(p + 1, sK1, sV1, sK0, sV0);
   }
-  if (q_valid) mfma_store_out<DH>(acc, out + (size_t)row * ldo + h * DH, hi);
+  // every step ends on a barrier, so no page buffer is read any more: waves
+  // 0-1 park their output rows in sK0, waves 2-3 in sK1
+  mfma_store_out_staged<DH>(acc, (wave < 2 ? sK0 : sK1) + (wave & 1) * 32 * DH, out, ldo, h * DH, lane,
+                            tile.q_begin + wave * 32, tile.q_count - wave * 32, rq.qa_n, rq.qa_row, rq.qb_row);
 }
 
 // ============================================================================
@@ -318,7 +341,6 @@ __global__ __launch_bounds__(256, 2) void self_attn_mfma(const bf16* __restrict_
   const int ld = 3 * d;
   const int qi = wave * 32 + l32;
   const bool wave_active = wave * 32 < tile.q_count;
-  const bool q_valid = qi < tile.q_count;
   const int i = tile.q_begin + min(qi, tile.q_count - 1);
   bool is_cand;
   int row;
@@ -336,6 +358,20 @@ __global__ __launch_bounds__(256, 2) void self_attn_mfma(const bf16* __restrict_
     const bf16* qr = qkv + (size_t)row * ld + h * DH + 8 * hi;
 #pragma unroll
     for (int kk = 0; kk < DH / 16; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qr + 16 * kk);
+  }
+  // a candidate's own key and value, fetched now so that their latency
+  // overlaps the serving keys
+  bf16x8 kown[DH / 16];
+  bf16x4 vown[DH / 32][4];
+  if (is_cand) {
+    const bf16* kr = qkv + (size_t)row * ld + d + h * DH + 8 * hi;
+#pragma unroll
+    for (int kk = 0; kk < DH / 16; ++kk) kown[kk] = *reinterpret_cast<const bf16x8*>(kr + 16 * kk);
+    const bf16* vr = qkv + (size_t)row * ld + 2 * d + h * DH + 4 * hi;
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) vown[db][gq] = *reinterpret_cast<const bf16x4*>(vr + 32 * db + 8 * gq);
   }
   MfmaAcc<DH> acc;
   acc.init();
@@ -380,11 +416,10 @@ __global__ __launch_bounds__(256, 2) void self_attn_mfma(const bf16* __restrict_
   if (is_cand) {
     // the candidate's own key: dot over this lane's half of the features, then
     // the other half from lane l ^ 32 (same query)
-    const bf16* kr = qkv + (size_t)row * ld + d + h * DH + 8 * hi;
     float dot = 0.f;
 #pragma unroll
     for (int kk = 0; kk < DH / 16; ++kk) {
-      const bf16x8 kv = *reinterpret_cast<const bf16x8*>(kr + 16 * kk);
+      const bf16x8 kv = kown[kk];
 #pragma unroll
       for (int t = 0; t < 8; ++t) dot = fmaf((float)qf[kk][t], (float)kv[t], dot);
     }
@@ -394,17 +429,46 @@ __global__ __launch_bounds__(256, 2) void self_attn_mfma(const bf16* __restrict_
     const float pself = exp2f((dot - m_new) * scale_log2);
     acc.l = acc.l * alpha + pself;
     acc.m = m_new;
-    const bf16* vr = qkv + (size_t)row * ld + 2 * d + h * DH + 4 * hi;
 #pragma unroll
     for (int db = 0; db < DH / 32; ++db)
 #pragma unroll
       for (int gq = 0; gq < 4; ++gq) {
-        const bf16x4 v4 = *reinterpret_cast<const bf16x4*>(vr + 32 * db + 8 * gq);
+        const bf16x4 v4 = vown[db][gq];
 #pragma unroll
         for (int t = 0; t < 4; ++t) acc.o[db][4 * gq + t] = fmaf(pself, (float)v4[t], acc.o[db][4 * gq + t] * alpha);
       }
   }
-  if (q_valid) mfma_store_out<DH>(acc, out + (size_t)row * d + h * DH, hi);
+  // The K/V tiles are free now (the loop ended on a barrier): waves 0-1 park
+  // their output rows in sK, waves 2-3 in sV, and store them as
+  // mfma_store_out_staged does (written out here: the helper's form of the
+  // row mapping costs this kernel four spilled registers).
+  constexpr int UPR = DH / 8;
+  auto swz = [](int r) { return UPR == 16 ? (r & 15) : ((r >> 1) & 7); };
+  bf16* stage = (wave < 2 ? sK : sV) + (wave & 1) * 32 * DH;
+  {
+    const float inv = acc.l > 0.f ? 1.f / acc.l : 0.f;
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        bf16x4 w;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w[t] = (bf16)(acc.o[db][4 * gq + t] * inv);
+        *reinterpret_cast<bf16x4*>(stage + l32 * DH + (((4 * db + gq) ^ swz(l32)) << 3) + 4 * hi) = w;
+      }
+  }
+  constexpr int RPI = 64 / UPR;  // rows per read instruction
+#pragma unroll
+  for (int k = 0; k < 32 / RPI; ++k) {
+    const int r = k * RPI + lane / UPR, q = lane % UPR;
+    const bf16x8 v = *reinterpret_cast<const bf16x8*>(stage + r * DH + ((q ^ swz(r)) << 3));
+    const int qr = wave * 32 + r;
+    if (qr < tile.q_count) {
+      const int ir = tile.q_begin + qr;
+      const int orow = cand_only ? rq.c_row + ir : (ir >= rq.S ? rq.c_row + (ir - rq.S) : rq.s_row + ir);
+      *reinterpret_cast<bf16x8*>(out + (size_t)orow * d + h * DH + q * 8) = v;
+    }
+  }
 }
 
 // ============================================================================
