@@ -1070,14 +1070,22 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
   char* O = cv.take<char*>(M64 * d * es);
   char* Y = cv.take<char*>(M64 * d * es);
   char* Hf = cv.take<char*>(M64 * F * es);
-  TX_LAUNCH(K_COPY, 0, 2.0 * M64 * d * es, [&]() -> hipError_t {
-    if (Ms) {
-      hipError_t e = hipMemcpyAsync(T, xs + (size_t)so[a] * d * es, (size_t)Ms * d * es, hipMemcpyDeviceToDevice, st);
-      if (e != hipSuccess) return e;
-    }
-    return hipMemcpyAsync(T + (size_t)Ms * d * es, xc + (size_t)co[a] * d * es, (size_t)Mc * d * es,
-                          hipMemcpyDeviceToDevice, st);
-  }());
+  // The first layer reads the serving and candidate tokens where they are
+  // (its QKV GEMM and the self-attention output GEMM's residual run once per
+  // token array) when the bf16 GEMMs can take them (16-byte aligned rows);
+  // otherwise they are copied into T, where the later layers' input lives.
+  const char* Xs = xs + (size_t)so[a] * d * es;
+  const char* Xc = xc + (size_t)co[a] * d * es;
+  const bool direct =
+      !bf || ((Ms == 0 || (uintptr_t)Xs % 16 == 0) && (uintptr_t)Xc % 16 == 0 && ((size_t)d * es) % 16 == 0);
+  if (!direct)
+    TX_LAUNCH(K_COPY, 0, 2.0 * M64 * d * es, [&]() -> hipError_t {
+      if (Ms) {
+        hipError_t e = hipMemcpyAsync(T, Xs, (size_t)Ms * d * es, hipMemcpyDeviceToDevice, st);
+        if (e != hipSuccess) return e;
+      }
+      return hipMemcpyAsync(T + (size_t)Ms * d * es, Xc, (size_t)Mc * d * es, hipMemcpyDeviceToDevice, st);
+    }());
   const float eps = m->cfg.ln_eps;
   const double dd = d, esd = (double)es;
   // algorithmic work of the attention launches: (query, key) pairs and cache bytes
@@ -1110,12 +1118,26 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
     };
     auto q = gf(Md, 3 * dd, dd, 0), o = gf(Mrd, dd, dd, 1), xq = gf(Mrd, dd, dd, 0), xo = gf(Mrd, dd, dd, 1),
          f1 = gf(Mrd, F, dd, 0), f2 = gf(Mrd, dd, F, 1);
-    TX_LAUNCH(K_GEMM_QKV, q.first, q.second,
-              launch_gemm(bf, T, d, L.qkv.w, L.qkv.b, nullptr, 0, QKV, 3 * d, M, 3 * d, d, EPI_BIAS, st));
+    // layer input rows r0 .. M - 1: T, or the token arrays in place (first layer)
+    const bool in_place = l == 0 && direct;
+    TX_LAUNCH(K_GEMM_QKV, q.first, q.second, [&]() -> hipError_t {
+      if (!in_place) return launch_gemm(bf, T, d, L.qkv.w, L.qkv.b, nullptr, 0, QKV, 3 * d, M, 3 * d, d, EPI_BIAS, st);
+      hipError_t e = launch_gemm(bf, Xs, d, L.qkv.w, L.qkv.b, nullptr, 0, QKV, 3 * d, (int)Ms, 3 * d, d, EPI_BIAS, st);
+      if (e != hipSuccess) return e;
+      return launch_gemm(bf, Xc, d, L.qkv.w, L.qkv.b, nullptr, 0, QKV + (size_t)Ms * 3 * d * es, 3 * d, (int)Mc,
+                         3 * d, d, EPI_BIAS, st);
+    }());
     TX_LAUNCH(K_SELF_ATTN, 4 * dd * (last ? self_cand : self_full), esd * (3 * Md * dd + Mrd * dd),
               launch_self_attention(bf, QKV, d, H, A, (const SelfReq*)(ws + o_sreq), stl, n_st, last, st));
-    TX_LAUNCH(K_GEMM_O, o.first, o.second,
-              launch_gemm(bf, A + ro, d, L.o.w, L.o.b, T + ro, d, Y + ro, d, Mr, d, d, EPI_BIAS_RESID, st));
+    TX_LAUNCH(K_GEMM_O, o.first, o.second, [&]() -> hipError_t {
+      if (!in_place) return launch_gemm(bf, A + ro, d, L.o.w, L.o.b, T + ro, d, Y + ro, d, Mr, d, d, EPI_BIAS_RESID, st);
+      const size_t cs = (size_t)Ms * d * es;  // candidate rows start here in A and Y
+      if (r0 == 0) {
+        hipError_t e = launch_gemm(bf, A, d, L.o.w, L.o.b, Xs, d, Y, d, (int)Ms, d, d, EPI_BIAS_RESID, st);
+        if (e != hipSuccess) return e;
+      }
+      return launch_gemm(bf, A + cs, d, L.o.w, L.o.b, Xc, d, Y + cs, d, (int)Mc, d, d, EPI_BIAS_RESID, st);
+    }());
     TX_LAUNCH(K_LAYERNORM, 0, 2 * Mrd * dd * esd, launch_layernorm(bf, Y + ro, T + ro, L.ln1g, L.ln1b, Mr, d, eps, st));
     TX_LAUNCH(K_GEMM_XQ, xq.first, xq.second,
               launch_gemm(bf, T + ro, d, L.xq.w, L.xq.b, nullptr, 0, A + ro, d, Mr, d, d, EPI_BIAS, st));
