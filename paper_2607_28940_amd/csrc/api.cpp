@@ -625,8 +625,10 @@ struct Meta {
 size_t meta_bound(int n_req, int64_t rows, int64_t max_rows, int H) {
   const int64_t tiles = (int64_t)H * (rows / 32 + n_req + 1) + 8 * (max_rows / 32 + 2);
   const int64_t pool_chunks = rows / 64 + n_req + 1;
+  const int64_t page_tiles = rows / kPage + n_req + 1;  // each request adds at most one partial page
   return align_up(8192 + (size_t)n_req * 160 + (size_t)tiles * sizeof(AttnTile) * 6 +
-                  (size_t)pool_chunks * sizeof(PoolChunk) + (size_t)n_req * sizeof(PoolReq));
+                  (size_t)pool_chunks * sizeof(PoolChunk) + (size_t)n_req * sizeof(PoolReq) +
+                  (size_t)page_tiles * sizeof(ScatterTile));
 }
 
 // Attention worklist: tiles of q_block queries for every (request, head),
@@ -815,13 +817,21 @@ int run_encoder_pass(tx_kv_cache* c, const char* X, int64_t rows, const std::vec
       preqs.push_back({c0, (int)chunks.size() - c0, s.slot, s.pos0 == 0 ? 1 : 0});
     }
   }
+  // cache pages written by this pass, split per request
+  std::vector<ScatterTile> ptiles;
+  for (const ScatterReq& s : sreqs)
+    for (int p = s.pos0 / kPage; p * kPage < s.pos0 + s.n; ++p) {
+      const int t0 = std::max(s.pos0, p * kPage) - p * kPage, t1 = std::min(s.pos0 + s.n, (p + 1) * kPage) - p * kPage;
+      ptiles.push_back(ScatterTile{s.slot, p, t0, t1, s.row0 + (p * kPage + t0 - s.pos0)});
+    }
   Meta meta;
-  const size_t o_sreq = meta.put(sreqs), o_areq = meta.put(areqs), o_tiles = meta.put(tiles);
-  const size_t o_chunks = meta.put(chunks), o_preqs = meta.put(preqs);
+  const size_t o_areq = meta.put(areqs), o_tiles = meta.put(tiles);
+  const size_t o_chunks = meta.put(chunks), o_preqs = meta.put(preqs), o_ptiles = meta.put(ptiles);
   const size_t mb = meta_bound(n, rows, mx, m->H);
   if (meta.buf.size() > mb) return fail(TX_E_NOMEM, "internal: metadata %zu > bound %zu", meta.buf.size(), mb);
   TX_HIP(c->st.upload(ws, meta.buf.data(), meta.buf.size(), st));
-  const ScatterReq* d_sreq = (const ScatterReq*)(ws + o_sreq);
+  const ScatterTile* d_ptiles = (const ScatterTile*)(ws + o_ptiles);
+  const int n_ptiles = (int)ptiles.size();
   const AttnReq* d_areq = (const AttnReq*)(ws + o_areq);
   const AttnTile* d_tiles = (const AttnTile*)(ws + o_tiles);
   Carver cv(ws + mb);
@@ -853,8 +863,8 @@ int run_encoder_pass(tx_kv_cache* c, const char* X, int64_t rows, const std::vec
     TX_LAUNCH(K_ENC_GEMM, g1.first, g1.second,
               launch_gemm(bf, in, d, L.qkv.w, L.qkv.b, nullptr, 0, QKV, 3 * d, M, 3 * d, d, EPI_BIAS, st));
     TX_LAUNCH(K_SCATTER, 0, 4 * Md * dd * esd,
-              launch_scatter_kv(bf, QKV + d * es, 3 * d, 1, e, c->pool, c->d_table, c->max_pages, c->geom, d_sreq, n,
-                                M, st));
+              launch_scatter_kv(bf, QKV + d * es, 3 * d, 1, e, c->pool, c->d_table, c->max_pages, c->geom, d_ptiles,
+                                n_ptiles, st));
     TX_LAUNCH(K_ENC_ATTN, 4 * dd * attn_pairs, kv_bytes + 2 * Md * dd * esd,
               launch_paged_attention(bf, QKV, 3 * d, A, d, c->pool, c->d_table, c->max_pages, c->geom, e, d_areq,
                                      d_tiles, (int)tiles.size(), true, L.rel, m->R, qb, st));
@@ -874,8 +884,8 @@ int run_encoder_pass(tx_kv_cache* c, const char* X, int64_t rows, const std::vec
   TX_LAUNCH(K_XKV_GEMM, g5.first, g5.second,
             launch_gemm(bf, T, d, m->xkv.w, m->xkv.b, nullptr, 0, Hf, nkv, M, nkv, d, EPI_BIAS, st));
   TX_LAUNCH(K_SCATTER, 0, 2 * Md * nkv * esd,
-            launch_scatter_kv(bf, Hf, nkv, m->n_dec, m->n_enc, c->pool, c->d_table, c->max_pages, c->geom, d_sreq, n,
-                              M, st));
+            launch_scatter_kv(bf, Hf, nkv, m->n_dec, m->n_enc, c->pool, c->d_table, c->max_pages, c->geom, d_ptiles,
+                              n_ptiles, st));
   if (m->gpool) {
     // fold the new rows into each request's pooling state, then project the
     // pooled token with every decoder layer's cross K/V weights

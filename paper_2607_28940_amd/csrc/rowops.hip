@@ -187,60 +187,67 @@ hipError_t launch_layernorm_score(bool bf, const void* x, const float* g, const 
 }
 
 // ---------------------------------------------------------------- cache scatter
-// One thread per (row, layer, K|V, head, 8-feature chunk). The row's request is
-// found by binary search over the requests' first rows (ascending).
+// One block per (page tile, layer, head): positions t0 .. t1-1 of one page of
+// one request, source rows row .. row + t1 - t0 - 1. K rows are copied 16 bytes
+// per lane. The page keeps V transposed ([dh][kPage], columns in vt_col order),
+// so the V^T tile is assembled in LDS (starting from the page's current
+// contents when the tile covers only part of the page) and written back as
+// whole 16-byte pieces of its rows.
 template <typename T>
-__global__ __launch_bounds__(256) void scatter_kv(const T* __restrict__ src, int lds, int n_layers, int slot0,
-                                                  T* __restrict__ pool, const int32_t* __restrict__ page_table,
-                                                  int max_pages, PageGeom g, const ScatterReq* __restrict__ reqs,
-                                                  int n_req, int64_t n_items) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= n_items) return;
-  const int chunks = g.dh / 8;
-  const int per_row = n_layers * 2 * g.H * chunks;
-  const int row = (int)(idx / per_row);
-  int rem = (int)(idx % per_row);
-  const int ch = rem % chunks;
-  rem /= chunks;
-  const int h = rem % g.H;
-  rem /= g.H;
-  const int kind = rem & 1;
-  const int layer = rem >> 1;
-  int lo = 0, hi = n_req - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (reqs[mid].row0 <= row) lo = mid;
-    else hi = mid - 1;
+__global__ __launch_bounds__(256) void scatter_pages(const T* __restrict__ src, int lds, int slot0,
+                                                     T* __restrict__ pool, const int32_t* __restrict__ page_table,
+                                                     int max_pages, PageGeom g, const ScatterTile* __restrict__ tiles) {
+  constexpr int VEC = 16 / sizeof(T);  // elements per 16 bytes
+  constexpr int LDP = kPage + 2;       // padded V^T row in LDS
+  __shared__ T sv[128 * LDP];
+  const ScatterTile tl = tiles[blockIdx.x];
+  const int layer = blockIdx.y / g.H, h = blockIdx.y % g.H;
+  const int d = g.H * g.dh, dh = g.dh, cpr = dh / VEC, n = tl.t1 - tl.t0;
+  T* base = pool + (size_t)page_table[(size_t)tl.slot * max_pages + tl.page] * g.page_elems;
+  T* kdst = base + g.k_off(slot0 + layer, h);
+  T* vdst = base + g.v_off(slot0 + layer, h);
+  const T* ksrc = src + (size_t)tl.row * lds + (size_t)layer * 2 * d + h * dh;
+  const T* vsrc = ksrc + d;
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  for (int c = threadIdx.x; c < n * cpr; c += 256) {
+    const int t = c / cpr, ch = c % cpr;
+    *reinterpret_cast<u32x4*>(kdst + (size_t)(tl.t0 + t) * dh + ch * VEC) =
+        *reinterpret_cast<const u32x4*>(ksrc + (size_t)t * lds + ch * VEC);
   }
-  const ScatterReq rq = reqs[lo];
-  const int pos = rq.pos0 + (row - rq.row0);
-  const int d = g.H * g.dh;
-  const T* s = src + (size_t)row * lds + (size_t)layer * 2 * d + kind * d + h * g.dh + ch * 8;
-  T* base = pool + (size_t)page_table[(size_t)rq.slot * max_pages + pos / kPage] * g.page_elems;
-  const int t = pos % kPage;
-  if (kind == 0) {
-    T* dst = base + g.k_off(slot0 + layer, h) + (size_t)t * g.dh + ch * 8;
+  constexpr int RC = kPage / VEC;  // 16-byte pieces per V^T row
+  if (n < kPage)
+    for (int c = threadIdx.x; c < dh * RC; c += 256) {
+      const int r = c / RC, q = c % RC;
+      *reinterpret_cast<u32x4*>(&sv[r * LDP + q * VEC]) = *reinterpret_cast<const u32x4*>(vdst + (size_t)r * kPage + q * VEC);
+    }
+  __syncthreads();
+  for (int c = threadIdx.x; c < n * cpr; c += 256) {
+    const int t = c / cpr, ch = c % cpr;
+    const u32x4 raw = *reinterpret_cast<const u32x4*>(vsrc + (size_t)t * lds + ch * VEC);
+    const T* v = reinterpret_cast<const T*>(&raw);
+    const int col = vt_col(tl.t0 + t);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) dst[e] = s[e];
-  } else {
-    T* dst = base + g.v_off(slot0 + layer, h) + (size_t)(ch * 8) * kPage + vt_col(t);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) dst[(size_t)e * kPage] = s[e];
+    for (int e = 0; e < VEC; ++e) sv[(ch * VEC + e) * LDP + col] = v[e];
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < dh * RC; c += 256) {
+    const int r = c / RC, q = c % RC;
+    *reinterpret_cast<u32x4*>(vdst + (size_t)r * kPage + q * VEC) = *reinterpret_cast<const u32x4*>(&sv[r * LDP + q * VEC]);
   }
 }
 
 hipError_t launch_scatter_kv(bool bf, const void* src, int lds, int n_layers, int slot0, void* pool,
-                             const int32_t* page_table, int max_pages, PageGeom g, const ScatterReq* reqs, int n_req,
-                             int n_rows, hipStream_t s) {
-  if (n_rows <= 0 || n_req <= 0) return hipSuccess;
-  const int64_t n_items = (int64_t)n_rows * n_layers * 2 * g.H * (g.dh / 8);
-  const int64_t blocks = (n_items + 255) / 256;
+                             const int32_t* page_table, int max_pages, PageGeom g, const ScatterTile* tiles,
+                             int n_tiles, hipStream_t s) {
+  if (n_tiles <= 0 || n_layers <= 0) return hipSuccess;
+  if (g.dh > 128 || g.dh % 8 != 0 || lds % 8 != 0) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)n_tiles, (unsigned)(n_layers * g.H));
   if (bf)
-    scatter_kv<bf16><<<(unsigned)blocks, 256, 0, s>>>((const bf16*)src, lds, n_layers, slot0, (bf16*)pool, page_table,
-                                                      max_pages, g, reqs, n_req, n_items);
+    scatter_pages<bf16><<<grid, 256, 0, s>>>((const bf16*)src, lds, slot0, (bf16*)pool, page_table, max_pages, g,
+                                             tiles);
   else
-    scatter_kv<float><<<(unsigned)blocks, 256, 0, s>>>((const float*)src, lds, n_layers, slot0, (float*)pool,
-                                                       page_table, max_pages, g, reqs, n_req, n_items);
+    scatter_pages<float><<<grid, 256, 0, s>>>((const float*)src, lds, slot0, (float*)pool, page_table, max_pages, g,
+                                              tiles);
   return hipGetLastError();
 }
 

@@ -50,6 +50,12 @@ struct ScatterReq {
   int32_t row0, n, pos0, slot;
 };
 
+// Part of one cache page written by a scatter: positions t0 .. t1-1 of page
+// `page` of request slot `slot`, position t0 coming from source row `row`.
+struct ScatterTile {
+  int32_t slot, page, t0, t1, row;
+};
+
 // Attention pooling work: rows row0 .. row0+n-1 (n <= 64) of the encoded
 // matrix, one chunk of the request at index `req` of the pass.
 struct PoolChunk {
@@ -115,10 +121,11 @@ hipError_t launch_self_attention(bool bf, const void* qkv, int d, int H, void* o
 int self_attention_q_block(bool bf, int dh);
 
 // Write K and V columns of src (per layer: K in cols [l*2d, l*2d+d), V in
-// [l*2d+d, l*2d+2d); ld = lds) into the pages of layer slots slot0 .. slot0+n_layers-1.
+// [l*2d+d, l*2d+2d); ld = lds) into the pages of layer slots
+// slot0 .. slot0+n_layers-1, one page tile (page_tiles) at a time.
 hipError_t launch_scatter_kv(bool bf, const void* src, int lds, int n_layers, int slot0, void* pool,
-                             const int32_t* page_table, int max_pages, PageGeom g, const ScatterReq* reqs,
-                             int n_req, int n_rows, hipStream_t s);
+                             const int32_t* page_table, int max_pages, PageGeom g, const ScatterTile* tiles,
+                             int n_tiles, hipStream_t s);
 // Export one cached tensor (K or V of a layer slot) of a request into a dense
 // [len][H*dh] matrix.
 hipError_t launch_export_kv(bool bf, const void* pool, const int32_t* page_row, PageGeom g, int layer_slot, int is_v,
