@@ -1082,12 +1082,15 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
   char* Hf = cv.take<char*>(M64 * F * es);
   // The first layer reads the serving and candidate tokens where they are
   // (its QKV GEMM and the self-attention output GEMM's residual run once per
-  // token array) when the bf16 GEMMs can take them (16-byte aligned rows);
-  // otherwise they are copied into T, where the later layers' input lives.
+  // token array) when the bf16 GEMMs can take them (16-byte aligned rows) and
+  // both arrays fill the GPU on their own (8192 rows or more: 32 row tiles
+  // of the persistent GEMM); otherwise they are copied into T, where the
+  // later layers' input lives.
   const char* Xs = xs + (size_t)so[a] * d * es;
   const char* Xc = xc + (size_t)co[a] * d * es;
-  const bool direct =
-      !bf || ((Ms == 0 || (uintptr_t)Xs % 16 == 0) && (uintptr_t)Xc % 16 == 0 && ((size_t)d * es) % 16 == 0);
+  const bool direct = (Ms == 0 || Ms >= 8192) && Mc >= 8192 &&
+                      (!bf || ((Ms == 0 || (uintptr_t)Xs % 16 == 0) && (uintptr_t)Xc % 16 == 0 &&
+                               ((size_t)d * es) % 16 == 0));
   if (!direct)
     TX_LAUNCH(K_COPY, 0, 2.0 * M64 * d * es, [&]() -> hipError_t {
       if (Ms) {
