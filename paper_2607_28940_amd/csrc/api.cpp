@@ -796,7 +796,6 @@ int run_encoder_pass(tx_kv_cache* c, const char* X, int64_t rows, const std::vec
   const tx_model* m = c->m;
   const bool bf = m->bf;
   const int d = m->d, F = m->F, n = (int)sreqs.size();
-  const int qb = paged_attention_q_block(bf, m->dh);
   std::vector<AttnReq> areqs(n);
   int64_t mx = 0;
   for (int i = 0; i < n; ++i) {
@@ -804,6 +803,10 @@ int run_encoder_pass(tx_kv_cache* c, const char* X, int64_t rows, const std::vec
     areqs[i] = AttnReq{s.row0, s.n, 0, 0, s.pos0 + s.n, s.pos0, s.slot, 0};
     mx = std::max<int64_t>(mx, s.n);
   }
+  // a few new tokens per request (an append): one wave per (request, head)
+  // streams the cached pages through registers
+  const int qb = (mx <= kDecodeQBlock && paged_attention_decode_ok(bf, m->dh, m->R)) ? kDecodeQBlock
+                                                                                 : paged_attention_q_block(bf, m->dh);
   std::vector<AttnTile> tiles;
   attn_tiles(areqs, m->H, qb, true, tiles);
   // global-token pooling: 64-row chunks of each request's new rows

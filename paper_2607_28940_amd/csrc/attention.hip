@@ -63,29 +63,32 @@ __device__ __forceinline__ int v_frag(int row, int slot) {
   return SWZ ? row * 64 + ((slot ^ ((row >> 1) & 7)) << 3) : row * VLD + (slot << 3);
 }
 
-template <int DH, int KLD, int VLD, class Mask, bool SWZ = false>
-__device__ __forceinline__ void mfma_attend_tile(const bf16* __restrict__ sK, const bf16* __restrict__ sV,
-                                                 const bf16x8 (&qf)[DH / 16], MfmaAcc<DH>& acc, float scale_log2,
-                                                 int l32, int hi, bool masked, Mask mask) {
+// The tile arithmetic takes its operands from fragment sources:
+// kfrag(kb, kk) is K row kb * 32 + l32, features 16 kk + 8 hi .. + 7;
+// vfrag(ks, db) is V^T row 32 db + l32, stored columns
+// 32 (ks / 2) + 16 (ks % 2) + 8 hi .. + 7. FROM_LDS adds scheduling hints
+// for fragments read from LDS.
+template <int DH, bool FROM_LDS, class KFrag, class VFrag, class Mask>
+__device__ __forceinline__ void mfma_attend_frags(KFrag kfrag, VFrag vfrag, const bf16x8 (&qf)[DH / 16],
+                                                  MfmaAcc<DH>& acc, float scale_log2, int hi, bool masked, Mask mask) {
   floatx16 s[2];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) s[kb][v] = 0.f;
 #pragma unroll
-    for (int kk = 0; kk < DH / 16; ++kk) {
-      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&sK[k_frag<DH, KLD, SWZ>(kb * 32 + l32, 2 * kk + hi)]);
-      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
-    }
+    for (int kk = 0; kk < DH / 16; ++kk) s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kfrag(kb, kk), qf[kk], s[kb], 0, 0, 0);
   }
-  // keep four K fragment reads in flight ahead of the MFMA that uses them
-  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+  if (FROM_LDS) {
+    // keep four K fragment reads in flight ahead of the MFMA that uses them
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-  for (int g = 0; g < DH / 8 - 4; ++g) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    for (int g = 0; g < DH / 8 - 4; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
   }
-  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
   if (masked) {  // wave-uniform
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -132,13 +135,24 @@ __device__ __forceinline__ void mfma_attend_tile(const bf16* __restrict__ sK, co
     bf16x8 pf;
 #pragma unroll
     for (int t = 0; t < 8; ++t) pf[t] = (bf16)s[kb][8 * half + t];
-    const int kbase = kb * 32 + 16 * half + 8 * hi;  // in the V^T tile's permuted key order
 #pragma unroll
-    for (int db = 0; db < DH / 32; ++db) {
-      const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&sV[v_frag<VLD, SWZ>(32 * db + l32, kbase >> 3)]);
-      acc.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc.o[db], 0, 0, 0);
-    }
+    for (int db = 0; db < DH / 32; ++db) acc.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(ks, db), pf, acc.o[db], 0, 0, 0);
   }
+}
+
+// The same tile with K and V^T staged in LDS.
+template <int DH, int KLD, int VLD, class Mask, bool SWZ = false>
+__device__ __forceinline__ void mfma_attend_tile(const bf16* __restrict__ sK, const bf16* __restrict__ sV,
+                                                 const bf16x8 (&qf)[DH / 16], MfmaAcc<DH>& acc, float scale_log2,
+                                                 int l32, int hi, bool masked, Mask mask) {
+  auto kfrag = [&](int kb, int kk) {
+    return *reinterpret_cast<const bf16x8*>(&sK[k_frag<DH, KLD, SWZ>(kb * 32 + l32, 2 * kk + hi)]);
+  };
+  auto vfrag = [&](int ks, int db) {
+    const int kbase = (ks >> 1) * 32 + 16 * (ks & 1) + 8 * hi;  // in the V^T tile's permuted key order
+    return *reinterpret_cast<const bf16x8*>(&sV[v_frag<VLD, SWZ>(32 * db + l32, kbase >> 3)]);
+  };
+  mfma_attend_frags<DH, true>(kfrag, vfrag, qf, acc, scale_log2, hi, masked, mask);
 }
 
 // Normalises the wave's 32 output rows, parks them in LDS (stage: 32 x DH
@@ -316,6 +330,141 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
   // 0-1 park their output rows in sK0, waves 2-3 in sK1
   mfma_store_out_staged<DH>(acc, (wave < 2 ? sK0 : sK1) + (wave & 1) * 32 * DH, out, ldo, h * DH, lane,
                             tile.q_begin + wave * 32, tile.q_count - wave * 32, rq.qa_n, rq.qa_row, rq.qb_row);
+}
+
+// ============================================================================
+// bf16 paged attention for few queries per (request, head): one wave per tile
+// of at most 32 queries, four independent tiles per block, no LDS. With no
+// other wave to share a page there is nothing to stage it for: each lane
+// loads its K and V^T MFMA fragments straight from the page into registers,
+// the next page's while the current one is used (128 KB of pages in flight
+// per CU against 64 KB for the staged kernel), which is what a tile of the
+// incremental append (16 new tokens against thousands of cached ones) is
+// bound by.
+// ============================================================================
+template <int DH>
+struct PageFrags {
+  bf16x8 k[2][DH / 16];  // K rows kb * 32 + l32, features 16 kk + 8 hi
+  bf16x8 v[4][DH / 32];  // V^T rows 32 db + l32, stored columns 32 (ks / 2) + 16 (ks % 2) + 8 hi
+};
+
+template <int DH, bool CAUSAL>
+__global__ __launch_bounds__(256, 1) void paged_attn_decode(const bf16* __restrict__ q, int ldq, bf16* __restrict__ out,
+                                                            int ldo, const bf16* __restrict__ pool,
+                                                            const int32_t* __restrict__ page_table, int max_pages,
+                                                            PageGeom g, int layer_slot,
+                                                            const AttnReq* __restrict__ reqs,
+                                                            const AttnTile* __restrict__ tiles, int n_tiles,
+                                                            const float* __restrict__ rel, int R, float scale_log2) {
+  const int t_idx = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t_idx >= n_tiles) return;  // whole waves; the kernel has no block-wide barrier
+  const AttnTile tile = tiles[t_idx];
+  if (tile.q_count <= 0) return;
+  const AttnReq rq = reqs[tile.req];
+  const int h = tile.head, lane = threadIdx.x & 63, l32 = lane & 31, hi = lane >> 5;
+  const int i = tile.q_begin + min(l32, tile.q_count - 1);
+  const int row = i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
+  const int qpos = rq.pos0 + i;
+  const float bias_scale = kLog2e / scale_log2;
+
+  bf16x8 qf[DH / 16];
+  {
+    const bf16* qr = q + (size_t)row * ldq + h * DH + 8 * hi;
+#pragma unroll
+    for (int kk = 0; kk < DH / 16; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qr + 16 * kk);
+  }
+  MfmaAcc<DH> acc;
+  acc.init();
+
+  const int kv_len = rq.kv_len;
+  int n_pages = (kv_len + kPage - 1) / kPage;
+  if (CAUSAL) n_pages = min(n_pages, (rq.pos0 + tile.q_begin + tile.q_count - 1) / kPage + 1);
+  const int32_t* ptab = page_table + (size_t)rq.slot * max_pages;
+  // the head's relative-position table, per wave in LDS: the mask reads it
+  // without a vector-memory wait, which would also wait for the page in flight
+  __shared__ float s_rel[4][kDecodeMaxRel];
+  float* wrel = s_rel[threadIdx.x >> 6];
+  if (CAUSAL)
+    for (int j = lane; j < R; j += 64) wrel[j] = rel[h * R + j];
+
+  auto fetch = [&](int p, PageFrags<DH>& f) {
+    const bf16* base = pool + (size_t)ptab[p] * g.page_elems;
+    const bf16* kp = base + g.k_off(layer_slot, h) + (size_t)l32 * DH + 8 * hi;
+    const bf16* vp = base + g.v_off(layer_slot, h) + (size_t)l32 * kPage + 8 * hi;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int kk = 0; kk < DH / 16; ++kk)
+        f.k[kb][kk] = *reinterpret_cast<const bf16x8*>(kp + (size_t)kb * 32 * DH + 16 * kk);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int db = 0; db < DH / 32; ++db)
+        f.v[ks][db] = *reinterpret_cast<const bf16x8*>(vp + (size_t)db * 32 * kPage + 32 * (ks >> 1) + 16 * (ks & 1));
+  };
+  auto attend = [&](int p, PageFrags<DH>& f, bool tail) {
+    const int key0 = p * kPage;
+    auto mask = [&](int kl, float x) {
+      const int key = key0 + kl;
+      bool ok = key < kv_len;
+      if (CAUSAL) {
+        ok = ok && key <= qpos;
+        if (R > 0) x += wrel[min(max(qpos - key, 0), R - 1)] * bias_scale;
+      }
+      return ok ? x : -INFINITY;
+    };
+    mfma_attend_frags<DH, false>([&](int kb, int kk) { return f.k[kb][kk]; },
+                                 [&](int ks, int db) { return f.v[ks][db]; }, qf, acc, scale_log2, hi, CAUSAL || tail,
+                                 mask);
+  };
+  // keys past the request's length on the last page: V^T columns zeroed (the
+  // page may hold anything there; their logits are masked)
+  auto zero_tail = [&](int p, PageFrags<DH>& f) {
+    const int valid = kv_len - p * kPage;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+          if (vt_col(32 * (ks >> 1) + 16 * (ks & 1) + 8 * hi + t) >= valid) f.v[ks][db][t] = (bf16)0.f;
+  };
+  // full pages in pairs (page p + 1 travels while page p is used), then the
+  // remaining full page and the partial last page, if any
+  const int n_full = n_pages * kPage > kv_len ? n_pages - 1 : n_pages;
+  PageFrags<DH> fa, fb;
+  fetch(0, fa);
+  int p = 0;
+  for (; p + 1 < n_full; p += 2) {
+    fetch(p + 1, fb);
+    attend(p, fa, false);
+    if (p + 2 < n_pages) fetch(p + 2, fa);
+    attend(p + 1, fb, false);
+  }
+  if (p < n_full) {
+    if (p + 1 < n_pages) fetch(p + 1, fb);
+    attend(p, fa, false);
+    if (++p < n_pages) {
+      zero_tail(p, fb);
+      attend(p, fb, true);
+    }
+  } else if (p < n_pages) {
+    zero_tail(p, fa);
+    attend(p, fa, true);
+  }
+  if (l32 < tile.q_count) {
+    const float inv = acc.l > 0.f ? 1.f / acc.l : 0.f;
+    bf16* orow = out + (size_t)row * ldo + h * DH + 4 * hi;
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        bf16x4 w;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w[t] = (bf16)(acc.o[db][4 * gq + t] * inv);
+        *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * gq) = w;
+      }
+  }
 }
 
 // ============================================================================
@@ -555,6 +704,22 @@ hipError_t launch_paged_attention(bool bf, const void* q, int ldq, void* out, in
                                   const float* rel, int R, int q_block, hipStream_t s) {
   if (n_tiles <= 0) return hipSuccess;
   const float sl2 = kLog2e / sqrtf((float)g.dh);
+  if (q_block == kDecodeQBlock && paged_attention_decode_ok(bf, g.dh, R)) {
+    const bf16* qq = (const bf16*)q;
+    bf16* oo = (bf16*)out;
+    const bf16* pp = (const bf16*)pool;
+    const unsigned blocks = (unsigned)((n_tiles + 3) / 4);
+#define TX_PD(DH, CZ)                                                                                              \
+  paged_attn_decode<DH, CZ><<<blocks, 256, 0, s>>>(qq, ldq, oo, ldo, pp, page_table, max_pages, g, layer_slot, reqs, \
+                                                    tiles, n_tiles, rel, R, sl2)
+    if (g.dh == 64) {
+      if (causal) TX_PD(64, true); else TX_PD(64, false);
+    } else {
+      if (causal) TX_PD(128, true); else TX_PD(128, false);
+    }
+#undef TX_PD
+    return hipGetLastError();
+  }
   if (q_block != paged_attention_q_block(bf, g.dh)) return hipErrorInvalidValue;
   if (bf && (g.dh == 64 || g.dh == 128)) {
     const bf16* qq = (const bf16*)q;

@@ -113,7 +113,13 @@ hipError_t launch_paged_attention(bool bf, const void* q, int ldq, void* out, in
                                   const AttnReq* reqs, const AttnTile* tiles, int n_tiles, bool causal,
                                   const float* rel, int R, int q_block, hipStream_t s);
 // Query block (queries per tile) each attention kernel variant expects.
+// Tiles of kDecodeQBlock queries (bf16, dh 64 or 128) select the kernel that
+// streams pages into registers: for passes with at most that many queries per
+// (request, head), where no page is shared by several waves.
 int paged_attention_q_block(bool bf, int dh);
+constexpr int kDecodeQBlock = 32;
+constexpr int kDecodeMaxRel = 256;  // relative-position buckets the register kernel holds
+inline bool paged_attention_decode_ok(bool bf, int dh, int R) { return bf && (dh == 64 || dh == 128) && R <= kDecodeMaxRel; }
 
 // Decoder self-attention over the packed QKV matrix (ld 3d).
 hipError_t launch_self_attention(bool bf, const void* qkv, int d, int H, void* out, const SelfReq* reqs,
