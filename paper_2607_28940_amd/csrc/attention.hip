@@ -402,9 +402,16 @@ __global__ __launch_bounds__(256, 1) void paged_attn_decode(const bf16* __restri
       for (int db = 0; db < DH / 32; ++db)
         f.v[ks][db] = *reinterpret_cast<const bf16x8*>(vp + (size_t)db * 32 * kPage + 32 * (ks >> 1) + 16 * (ks & 1));
   };
+  // Causal pages whose every key lies at least R - 1 positions before the
+  // tile's first query are visible to all its queries with the bias at the
+  // last bucket: one added constant instead of the per-logit mask.
+  const int q_first = rq.pos0 + tile.q_begin;
+  const float far_bias = (CAUSAL && R > 0) ? wrel[R - 1] * bias_scale : 0.f;
   auto attend = [&](int p, PageFrags<DH>& f, bool tail) {
     const int key0 = p * kPage;
+    const bool far = CAUSAL && !tail && key0 + kPage - 1 + max(R - 1, 0) <= q_first;
     auto mask = [&](int kl, float x) {
+      if (far) return x + far_bias;
       const int key = key0 + kl;
       bool ok = key < kv_len;
       if (CAUSAL) {
@@ -414,8 +421,8 @@ __global__ __launch_bounds__(256, 1) void paged_attn_decode(const bf16* __restri
       return ok ? x : -INFINITY;
     };
     mfma_attend_frags<DH, false>([&](int kb, int kk) { return f.k[kb][kk]; },
-                                 [&](int ks, int db) { return f.v[ks][db]; }, qf, acc, scale_log2, hi, CAUSAL || tail,
-                                 mask);
+                                 [&](int ks, int db) { return f.v[ks][db]; }, qf, acc, scale_log2, hi,
+                                 tail || (CAUSAL && (!far || R > 0)), mask);
   };
   // keys past the request's length on the last page: V^T columns zeroed (the
   // page may hold anything there; their logits are masked)
