@@ -22,28 +22,25 @@
 
 namespace tx {
 
-// GELU(x) = x Phi(x). With u = |x|, Phi(-u) = erfc(u / sqrt 2) / 2 comes from
-// the Chebyshev fit of Press et al. (Numerical Recipes, erfcc; fractional
-// error below 1.2e-7 for every argument, so the negative tail keeps its
-// relative accuracy):
-//   erfc(z) = t exp(-z^2 + P(t)),  t = 1 / (1 + z/2),  z = u / sqrt 2,
-// evaluated as Phi(-u) = t 2^(P'(t) - (c u)^2) with P' = log2(e) P - 1 and
-// c^2 = log2(e) / 2 (change of base and the halving folded into the
-// coefficients). Then x Phi(x) = max(x, 0) - u Phi(-u) for either sign of x:
-// one reciprocal, one exp2 and 12 FMA-type operations.
+// GELU(x) = x Phi(x) = max(x, 0) - u Phi(-u) with u = |x|, for either sign
+// of x. Phi(-u) = erfc(u / sqrt 2) / 2, with erfc(z) = t exp(-z^2 + P(t)),
+// t = 1 / (1 + z / 2) (the form of Press et al., Numerical Recipes erfcc) and
+// P a degree-7 least-squares fit on Chebyshev nodes (gelu_fit.py; fractional
+// error below 7.4e-7 for every argument, so the negative tail keeps its
+// relative accuracy). Evaluated as Phi(-u) = t 2^(P'(t) - (c u)^2) with
+// P' = log2(e) P - 1 and c^2 = log2(e) / 2: one reciprocal, one exp2 and 10
+// FMA-type operations.
 __device__ __forceinline__ float gelu_erf(float x) {
   const float u = fabsf(x);
   const float t = __builtin_amdgcn_rcpf(fmaf(u, 0.35355339059327373f, 1.0f));
-  float p = 0.24651729790196045f;
-  p = fmaf(p, t, -1.1861149450768025f);
-  p = fmaf(p, t, 2.147474463933521f);
-  p = fmaf(p, t, -1.637753152343414f);
-  p = fmaf(p, t, 0.40232158165127635f);
-  p = fmaf(p, t, -0.2687568603388257f);
-  p = fmaf(p, t, 0.1396300565225048f);
-  p = fmaf(p, t, 0.5397006155284324f);
-  p = fmaf(p, t, 1.4427292039075317f);
-  p = fmaf(p, t, -2.825748218405333f);
+  float p = -0.2718776930163839f;
+  p = fmaf(p, t, 1.0879713150078754f);
+  p = fmaf(p, t, -1.449840280957486f);
+  p = fmaf(p, t, 0.5090884597583125f);
+  p = fmaf(p, t, -0.05895698505211376f);
+  p = fmaf(p, t, 0.5686708691445311f);
+  p = fmaf(p, t, 1.4406420004433174f);
+  p = fmaf(p, t, -2.825698746517148f);
   const float w = u * 0.8493218002880191f;
   const float q = t * __builtin_amdgcn_exp2f(fmaf(-w, w, p));  // Phi(-u)
   return fmaf(-u, q, fmaxf(x, 0.f));

@@ -1,22 +1,27 @@
 """The GEMM epilogue's GELU formula, checked on the CPU (no GPU needed).
 
 The FFN's activation is the exact erf GELU, x Phi(x) (Sec. 4.1.2). The HIP
-epilogue evaluates Phi(-|x|) = erfc(|x| / sqrt 2) / 2 from the Chebyshev fit
-of Press et al. (Numerical Recipes, erfcc) with the change to base 2 and the
-halving folded into its coefficients. This test reads the constants out of
-`gelu_erf` in the kernel source, evaluates the same formula in fp64 and
-compares it with scipy's erfc: a mistyped or wrongly rescaled coefficient, or
-a wrong sign in the final combination, shows up as an error far above the
-fit's 1.2e-7.
+epilogue evaluates Phi(-|x|) = erfc(|x| / sqrt 2) / 2 in the form of Press et
+al. (erfc(z) = t exp(-z^2 + P(t)), t = 1 / (1 + z / 2)) with P a degree-7 fit
+made by csrc/gelu_fit.py, the change to base 2 and the halving folded into
+its coefficients. This test reads the constants out of `gelu_erf` in the
+kernel source, checks that they are the fit script's, evaluates the formula
+in fp64 and compares it with scipy's erfc: a mistyped or wrongly rescaled
+coefficient, or a wrong sign in the final combination, shows up as an error
+far above the fit's 7.4e-7. (The kernel's fp32 constants and arithmetic add
+rounding of order 1e-6, up to ~1e-5 in the far negative tail |x| > 8 where
+the squared exponent is large; the bf16 output resolves 4e-3.)
 """
+import importlib.util
 import os
 import re
 
 import numpy as np
 from scipy.special import erfc
 
-SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2607_28940_amd", "csrc",
-                   "gemm.hip")
+CSRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2607_28940_amd", "csrc")
+SRC = os.path.join(CSRC, "gemm.hip")
+BOUND = 1e-6
 
 
 def _constants():
@@ -28,10 +33,10 @@ def _constants():
 
 def _formula(x):
     c = _constants()
-    # order in the source: t scale, 1.0, ten polynomial coefficients from the
-    # highest power down, the scale of the exponent's square
-    assert len(c) == 13, c
-    t_scale, one, poly, w_scale = c[0], c[1], c[2:12], c[12]
+    # order in the source: t scale, 1.0, eight polynomial coefficients from
+    # the highest power down, the scale of the exponent's square
+    assert len(c) == 11, c
+    t_scale, one, poly, w_scale = c[0], c[1], c[2:10], c[10]
     assert one == 1.0
     u = np.abs(x)
     t = 1.0 / (u * t_scale + one)
@@ -43,11 +48,21 @@ def _formula(x):
     return np.maximum(x, 0.0) - u * q, q
 
 
+def test_constants_are_the_fit():
+    spec = importlib.util.spec_from_file_location("gelu_fit", os.path.join(CSRC, "gelu_fit.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    coef, t_scale, w_scale = mod.fit()
+    c = _constants()
+    want = [t_scale, 1.0] + list(coef) + [w_scale]
+    assert np.allclose(c, want, rtol=1e-12, atol=0), (c, want)
+
+
 def test_phi_tail_relative_error():
     x = np.linspace(-14.0, 14.0, 400001)
     _, q = _formula(x)
     phi = 0.5 * erfc(np.abs(x) / np.sqrt(2.0))  # Phi(-|x|)
-    assert np.max(np.abs(q / phi - 1.0)) < 2e-7
+    assert np.max(np.abs(q / phi - 1.0)) < BOUND
 
 
 def test_gelu_relative_error():
@@ -55,5 +70,5 @@ def test_gelu_relative_error():
     g, _ = _formula(x)
     ref = 0.5 * x * erfc(-x / np.sqrt(2.0))
     nz = ref != 0
-    assert np.max(np.abs(g[nz] / ref[nz] - 1.0)) < 2e-7
+    assert np.max(np.abs(g[nz] / ref[nz] - 1.0)) < BOUND
     assert np.all(g[~nz] == 0.0)
