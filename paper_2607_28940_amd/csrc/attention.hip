@@ -711,7 +711,7 @@ hipError_t launch_paged_attention(bool bf, const void* q, int ldq, void* out, in
                                   const float* rel, int R, int q_block, hipStream_t s) {
   if (n_tiles <= 0) return hipSuccess;
   const float sl2 = kLog2e / sqrtf((float)g.dh);
-  if (q_block == kDecodeQBlock && paged_attention_decode_ok(bf, g.dh, R)) {
+  if (q_block == kDecodeQBlock && causal && paged_attention_decode_ok(bf, g.dh, R)) {
     const bf16* qq = (const bf16*)q;
     bf16* oo = (bf16*)out;
     const bf16* pp = (const bf16*)pool;
@@ -719,11 +719,7 @@ hipError_t launch_paged_attention(bool bf, const void* q, int ldq, void* out, in
 #define TX_PD(DH, CZ)                                                                                              \
   paged_attn_decode<DH, CZ><<<blocks, 256, 0, s>>>(qq, ldq, oo, ldo, pp, page_table, max_pages, g, layer_slot, reqs, \
                                                     tiles, n_tiles, rel, R, sl2)
-    if (g.dh == 64) {
-      if (causal) TX_PD(64, true); else TX_PD(64, false);
-    } else {
-      if (causal) TX_PD(128, true); else TX_PD(128, false);
-    }
+    if (g.dh == 64) TX_PD(64, true); else TX_PD(128, true);
 #undef TX_PD
     return hipGetLastError();
   }

@@ -113,9 +113,10 @@ hipError_t launch_paged_attention(bool bf, const void* q, int ldq, void* out, in
                                   const AttnReq* reqs, const AttnTile* tiles, int n_tiles, bool causal,
                                   const float* rel, int R, int q_block, hipStream_t s);
 // Query block (queries per tile) each attention kernel variant expects.
-// Tiles of kDecodeQBlock queries (bf16, dh 64 or 128) select the kernel that
-// streams pages into registers: for passes with at most that many queries per
-// (request, head), where no page is shared by several waves.
+// Causal tiles of kDecodeQBlock queries (bf16, dh 64 or 128, at most
+// kDecodeMaxRel relative-position buckets) select the kernel that streams
+// pages into registers: for encoder passes with at most that many new tokens
+// per request (appends), where no page is shared by several waves.
 int paged_attention_q_block(bool bf, int dh);
 constexpr int kDecodeQBlock = 32;
 constexpr int kDecodeMaxRel = 256;  // relative-position buckets the register kernel holds

@@ -120,10 +120,14 @@ def test_cache_contents_vs_oracle(O):
                 assert e < 5e-2, (r, part, layer, e)
 
 
-def test_append_equals_rebuild(O):
+@pytest.mark.parametrize("name,model", SMALL_BF16, ids=[m[0] for m in SMALL_BF16])
+def test_append_equals_rebuild(O, name, model):
     """App. D remark: appending events through the incremental encoder gives the
-    cache (and scores) of re-encoding the whole sequence."""
-    model = SMALL_BF16[0][1]
+    cache (and scores) of re-encoding the whole sequence. The appends (5, then
+    8 events per request) run the encoder's causal attention on the
+    register-streaming kernel (at most 32 new tokens per request), the rebuild
+    on the LDS-staged one; head widths 128 and 64, with and without the
+    relative-position bias."""
     wl = I.custom_workload(model, cfg_id=33, L=[60, 130], S=[6, 2], C=[9, 17], n_append=13)
     w = I.make_weights(model, ("sharp", "affine"))
     inc = DeviceCase(wl, w)
@@ -136,12 +140,12 @@ def test_append_equals_rebuild(O):
          for r in (0, 1)]
     full.cache.build([0, 1], full.dev(np.concatenate(X)), I.offsets([len(x) for x in X]))
     for r in (0, 1):
-        for part, nl in ((0, 2), (1, 2), (2, 2), (3, 2)):
-            for layer in range(nl):
+        for part in range(4):
+            for layer in range(model.n_enc_layers if part < 2 else model.n_dec_layers):
                 a = inc.cache.export(r, part, layer).float().cpu().numpy()
                 b = full.cache.export(r, part, layer).float().cpu().numpy()
                 e = tensor_err(a, b)
-                log(f"append vs rebuild r{r} part{part} layer{layer}: {e:.3e} exact={np.array_equal(a, b)}")
+                log(f"append vs rebuild {name} r{r} part{part} layer{layer}: {e:.3e} exact={np.array_equal(a, b)}")
                 assert e < 1e-2
     g_inc = np.concatenate(inc.score([0, 1]))
     g_full = np.concatenate(full.score([0, 1]))
@@ -149,7 +153,7 @@ def test_append_equals_rebuild(O):
     orc = O.Oracle(model, w)
     o = np.concatenate([oracle_request(orc, wl, r, append=True)[0] for r in (0, 1)])
     err = score_err(g_inc, o)
-    log(f"append scores vs oracle: {err}")
+    log(f"append scores vs oracle ({name}): {err}")
     check_err(err, BF16_TOL)
 
 
