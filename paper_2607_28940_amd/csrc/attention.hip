@@ -54,6 +54,19 @@ struct MfmaAcc {
 // rows of DH elements with 16-byte slot s of row r holding chunk s ^ (r mod
 // DH/8), V^T rows of 64 with slot s holding chunk s ^ ((r / 2) mod 8); both
 // keep the fragment reads of 8 consecutive rows on distinct banks.
+// Combine a value with the one lane l ^ 32 holds: v_permlane32_swap of two
+// copies leaves (x[l mod 32], x[32 + l mod 32]) in its two results on every
+// lane, so one VALU swap replaces an LDS round trip (ds_bpermute); max and
+// sum are symmetric, so both halves get the same bits.
+__device__ __forceinline__ float xor32_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xor32_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 template <int DH, int KLD, bool SWZ>
 __device__ __forceinline__ int k_frag(int row, int slot) {
   return SWZ ? row * DH + ((slot ^ (row & (DH / 8 - 1))) << 3) : row * KLD + (slot << 3);
@@ -100,7 +113,7 @@ __device__ __forceinline__ void mfma_attend_frags(KFrag kfrag, VFrag vfrag, cons
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kb][v]);
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  mx = xor32_max(mx);
   // Lazy reference max: probabilities are exp2((s - m) * scale) against a
   // reference m that only moves when this tile would push one above 2^8
   // (fine for fp32 sums and bf16 P); O and l are rescaled only then. The
@@ -127,7 +140,7 @@ __device__ __forceinline__ void mfma_attend_frags(KFrag kfrag, VFrag vfrag, cons
       s[kb][v] = e;
       rs += e;
     }
-  rs += __shfl_xor(rs, 32);
+  rs = xor32_sum(rs);
   acc.l += rs;
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
@@ -579,7 +592,7 @@ __global__ __launch_bounds__(256, 2) void self_attn_mfma(const bf16* __restrict_
 #pragma unroll
       for (int t = 0; t < 8; ++t) dot = fmaf((float)qf[kk][t], (float)kv[t], dot);
     }
-    dot += __shfl_xor(dot, 32);
+    dot = xor32_sum(dot);
     const float m_new = fmaxf(acc.m, dot);
     const float alpha = exp2f((acc.m - m_new) * scale_log2);
     const float pself = exp2f((dot - m_new) * scale_log2);
