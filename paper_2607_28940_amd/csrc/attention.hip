@@ -15,6 +15,7 @@
 // Softmax is the online (running max / running sum) form in fp32 in the base-2
 // domain: logits are scaled by log2(e) and exponentiated with exp2.
 #include "tx_internal.h"
+#include "wave_reduce.h"
 
 namespace tx {
 
@@ -54,19 +55,6 @@ struct MfmaAcc {
 // rows of DH elements with 16-byte slot s of row r holding chunk s ^ (r mod
 // DH/8), V^T rows of 64 with slot s holding chunk s ^ ((r / 2) mod 8); both
 // keep the fragment reads of 8 consecutive rows on distinct banks.
-// Combine a value with the one lane l ^ 32 holds: v_permlane32_swap of two
-// copies leaves (x[l mod 32], x[32 + l mod 32]) in its two results on every
-// lane, so one VALU swap replaces an LDS round trip (ds_bpermute); max and
-// sum are symmetric, so both halves get the same bits.
-__device__ __forceinline__ float xor32_max(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float xor32_sum(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
 template <int DH, int KLD, bool SWZ>
 __device__ __forceinline__ int k_frag(int row, int slot) {
   return SWZ ? row * DH + ((slot ^ (row & (DH / 8 - 1))) << 3) : row * KLD + (slot << 3);
@@ -694,8 +682,7 @@ __global__ __launch_bounds__(256) void paged_attn_plain(const T* __restrict__ q,
         float s = 0.f;
 #pragma unroll
         for (int e = 0; e < DP; ++e) s = fmaf(qv[e], sK[j][part * DP + e], s);
-        s += __shfl_xor(s, 1);
-        s += __shfl_xor(s, 2);
+        s = quad_sum(s);  // the query's four lanes
         s *= scale_log2;
         if (causal && R > 0) s += rel[h * R + min(qpos - key, R - 1)] * kLog2e;
         const float m_new = fmaxf(m_run, s);
@@ -805,8 +792,7 @@ __global__ __launch_bounds__(256) void self_attn_plain(const T* __restrict__ qkv
   }
   float m_run = -INFINITY, l_run = 0.f;
   auto consume = [&](float s, const float* vrow_part, int vstride) {
-    s += __shfl_xor(s, 1);
-    s += __shfl_xor(s, 2);
+    s = quad_sum(s);  // the query's four lanes
     s *= scale_log2;
     const float m_new = fmaxf(m_run, s);
     const float alpha = exp2f(m_run - m_new);

@@ -5,6 +5,7 @@
 //   scatter of projected K/V rows into
 //   the paged cache layout, cache export, and weight repacking.
 #include "tx_internal.h"
+#include "wave_reduce.h"
 
 #include <algorithm>
 
@@ -25,8 +26,7 @@ __device__ __forceinline__ void head_out(const float (&z)[CNT], int c0, int stri
 #pragma unroll
     for (int e = 0; e < CNT; ++e)
       if (e < cnt) dot += z[e] * w[c0 + e * stride];
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) dot += __shfl_xor(dot, o);
+    dot = wave_sum(dot);
     if (lane == 0) scores[row] = dot + b0[0];
     return;
   }
@@ -36,17 +36,14 @@ __device__ __forceinline__ void head_out(const float (&z)[CNT], int c0, int stri
 #pragma unroll
     for (int e = 0; e < CNT; ++e)
       if (e < cnt) dot += z[e] * w[(size_t)a * d + c0 + e * stride];
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) dot += __shfl_xor(dot, o);
+    dot = wave_sum(dot);
     if (lane == a) mine = dot + b0[a];
   }
   float mx = mine;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  mx = wave_max(mx);
   const float e = lane < n_act ? expf(mine - mx) : 0.f;
   float den = e;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) den += __shfl_xor(den, o);
+  den = wave_sum(den);
   if (lane < n_act) scores[(size_t)row * n_act + lane] = e / den;
 }
 
@@ -86,8 +83,7 @@ __global__ __launch_bounds__(256) void layernorm_rows(const T* __restrict__ x, T
     float sum = 0.f;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) sum += v[e];
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+    sum = wave_sum(sum);
     const float mean = sum / d;
     float sq = 0.f;
 #pragma unroll
@@ -95,8 +91,7 @@ __global__ __launch_bounds__(256) void layernorm_rows(const T* __restrict__ x, T
       const float t = v[e] - mean;
       sq += t * t;
     }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) sq += __shfl_xor(sq, o);
+    sq = wave_sum(sq);
     const float inv = rsqrtf(sq / d + eps);
     if (SCORE) {
       float z[EPL];
@@ -123,14 +118,14 @@ __global__ __launch_bounds__(256) void layernorm_rows_any(const T* __restrict__ 
   const T* xr = x + (size_t)row * d;
   float sum = 0.f;
   for (int c = lane; c < d; c += 64) sum += (float)xr[c];
-  for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+  sum = wave_sum(sum);
   const float mean = sum / d;
   float sq = 0.f;
   for (int c = lane; c < d; c += 64) {
     const float t = (float)xr[c] - mean;
     sq += t * t;
   }
-  for (int o = 32; o >= 1; o >>= 1) sq += __shfl_xor(sq, o);
+  sq = wave_sum(sq);
   const float inv = rsqrtf(sq / d + eps);
   if (!SCORE) {
     for (int c = lane; c < d; c += 64) y[(size_t)row * d + c] = (T)(((float)xr[c] - mean) * inv * g[c] + b[c]);

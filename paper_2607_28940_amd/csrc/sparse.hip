@@ -15,6 +15,7 @@
 // encoded rows once, and the attention touches at most 65 keys per query, so
 // these kernels use plain fp32 arithmetic rather than MFMA tiles.
 #include "tx_internal.h"
+#include "wave_reduce.h"
 
 namespace tx {
 
@@ -32,8 +33,7 @@ __global__ __launch_bounds__(256) void pool_partial(const T* __restrict__ H, int
     const T* h = H + (size_t)(ck.row0 + r) * d;
     float s = 0.f;
     for (int f = lane; f < d; f += 64) s = fmaf((float)h[f], w[f], s);
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    s = wave_sum(s);
     if (lane == 0) z[r] = s * zscale;
   }
   __syncthreads();
@@ -192,8 +192,7 @@ __global__ __launch_bounds__(256) void lg_cross_attn(const T* __restrict__ q, in
 #pragma unroll
       for (int c = 0; c < 4; ++c) s = fmaf(qv[4 * e + c], k4[c], s);
     }
-    s += __shfl_xor(s, 1);
-    s += __shfl_xor(s, 2);
+    s = quad_sum(s);  // the query's four lanes
     s *= scale_log2;
     const float m_new = fmaxf(m, s);
     const float alpha = __builtin_amdgcn_exp2f(m - m_new);  // 0 while m is -inf
