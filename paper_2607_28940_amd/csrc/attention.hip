@@ -335,13 +335,13 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
 
 // ============================================================================
 // bf16 paged attention for few queries per (request, head): one wave per tile
-// of at most 32 queries, four independent tiles per block, no LDS. With no
-// other wave to share a page there is nothing to stage it for: each lane
-// loads its K and V^T MFMA fragments straight from the page into registers,
-// the next page's while the current one is used (128 KB of pages in flight
-// per CU against 64 KB for the staged kernel), which is what a tile of the
-// incremental append (16 new tokens against thousands of cached ones) is
-// bound by.
+// of at most 32 queries, four independent tiles per block, pages not staged
+// in LDS. With no other wave to share a page there is nothing to stage it
+// for: each lane loads its K and V^T MFMA fragments straight from the page
+// into registers, the next page's while the current one is used (at d_h = 128
+// one wave per SIMD, 128 KB of pages in flight per CU against 64 KB for the
+// staged kernel), which is what a tile of the incremental append (16 new
+// tokens against thousands of cached ones) is bound by.
 // ============================================================================
 template <int DH>
 struct PageFrags {
