@@ -130,14 +130,27 @@ __device__ __forceinline__ void mfma_attend_frags(KFrag kfrag, VFrag vfrag, cons
     }
   rs = xor32_sum(rs);
   acc.l += rs;
+  bf16x8 pf[4];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    const int kb = ks >> 1, half = ks & 1;
-    bf16x8 pf;
+  for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-    for (int t = 0; t < 8; ++t) pf[t] = (bf16)s[kb][8 * half + t];
+    for (int t = 0; t < 8; ++t) pf[ks][t] = (bf16)s[ks >> 1][8 * (ks & 1) + t];
+  // from LDS: the V^T fragment reads start after the softmax and run four
+  // ahead of their MFMAs, as the K reads do, instead of all being hoisted
+  // above the softmax (which holds 64 more registers through it)
+  if (FROM_LDS) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int db = 0; db < DH / 32; ++db) acc.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(ks, db), pf, acc.o[db], 0, 0, 0);
+  for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db) acc.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(ks, db), pf[ks], acc.o[db], 0, 0, 0);
+  if (FROM_LDS) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int g = 0; g < DH / 8 - 4; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
   }
 }
 
@@ -198,7 +211,7 @@ __device__ __forceinline__ void mfma_store_out_staged(const MfmaAcc<DH>& acc, bf
 // A block of 4 waves serves up to 128 queries of one (request, head); each
 // wave owns 32 queries. For every 64-token page the block stages K [64][dh]
 // and V^T [dh][64] in LDS (double-buffered: the next page travels from HBM/L2
-// straight into LDS with global_load_lds while the current one is used, no
+// straight into LDS with buffer loads to LDS while the current one is used, no
 // register staging), so every K/V byte fetched from HBM/L2 feeds all queries
 // of the block. The page keeps V^T in the column order the PV MFMA wants; the
 // tiles are XOR-swizzled in LDS (the swizzle applied on the global side, since
@@ -223,8 +236,11 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
                                                            const AttnTile* __restrict__ tiles,
                                                            const float* __restrict__ rel, int R, float scale_log2) {
   constexpr int KLD = DH, VLD = 64;  // swizzled, unpadded tiles
-  __shared__ __attribute__((aligned(16))) bf16 sK0[64 * DH], sK1[64 * DH];
-  __shared__ __attribute__((aligned(16))) bf16 sV0[DH * 64], sV1[DH * 64];
+  // K page buffers 0, 1, then V^T page buffers 0, 1
+  __shared__ __attribute__((aligned(16))) bf16 sKV[4 * 64 * DH];
+  bf16* const sK0 = sKV;
+  bf16* const sK1 = sKV + 64 * DH;
+  bf16* const sV0 = sKV + 2 * 64 * DH;
 
   const AttnTile tile = tiles[blockIdx.x];
   if (tile.q_count <= 0) return;
@@ -259,26 +275,35 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
   }
   const int32_t* ptab = page_table + (size_t)rq.slot * max_pages;
 
-  // Pages travel HBM/L2 -> LDS with global_load_lds_dwordx4: each wave moves
-  // DH/32 KB of the K slab and as much of the V^T slab per page; lane l of a
-  // 1 KB load fills 16-byte slot l of it with the chunk the swizzle puts there.
-  // Page p+1 is requested while page p is used; every wave waits for its own
-  // loads before the page's closing barrier.
+  // Pages travel HBM/L2 -> LDS with buffer_load_dwordx4 ... lds: each wave
+  // moves DH/32 KB of the K slab and as much of the V^T slab per page; lane l
+  // of a 1 KB load fills 16-byte slot l of it with the chunk the swizzle puts
+  // there. The lanes' byte offsets within a slab are fixed, so they are
+  // computed once; per page only the slab bases (scalar) change. Page p+1 is
+  // requested while page p is used; every wave waits for its own loads before
+  // the page's closing barrier.
   typedef __attribute__((address_space(3))) void* lds_ptr_t;
+  uint32_t koff[DH / 32], voff[DH / 32];
+#pragma unroll
+  for (int u = 0; u < DH / 32; ++u) {
+    const int e = (wave + 4 * u) * 512 + lane * 8;  // first element of the lane's chunk of 1 KB piece wave + 4u
+    const int kr = e / DH, ks = (e % DH) >> 3;
+    const int vr = e >> 6, vs = (e & 63) >> 3;
+    koff[u] = 2u * (uint32_t)(kr * DH + ((ks ^ (kr & (DH / 8 - 1))) << 3));
+    voff[u] = 2u * (uint32_t)(vr * 64 + ((vs ^ ((vr >> 1) & 7)) << 3));
+  }
   auto dma = [&](int p, bf16* dK, bf16* dV) {
     const bf16* base = pool + (size_t)ptab[p] * g.page_elems;
-    const bf16* kp = base + g.k_off(layer_slot, h);
-    const bf16* vp = base + g.v_off(layer_slot, h);
+    // raw buffer resources over the two 64 x DH slabs (word 3 as CDNA wants it)
+    const __amdgpu_buffer_rsrc_t kr =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(base + g.k_off(layer_slot, h)), 0, 128 * DH, 0x00020000);
+    const __amdgpu_buffer_rsrc_t vr =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(base + g.v_off(layer_slot, h)), 0, 128 * DH, 0x00020000);
 #pragma unroll
     for (int u = 0; u < DH / 32; ++u) {
-      const int gi = wave * (DH / 32) + u;      // 1 KB piece of the slab
-      const int e = gi * 512 + lane * 8;        // its lane's first element
-      const int kr = e / DH, ks = (e % DH) >> 3;
-      __builtin_amdgcn_global_load_lds(kp + kr * DH + ((ks ^ (kr & (DH / 8 - 1))) << 3),
-                                       (lds_ptr_t)(dK + gi * 512), 16, 0, 0);
-      const int vr = e >> 6, vs = (e & 63) >> 3;
-      __builtin_amdgcn_global_load_lds(vp + vr * 64 + ((vs ^ ((vr >> 1) & 7)) << 3), (lds_ptr_t)(dV + gi * 512),
-                                       16, 0, 0);
+      const int gi = wave + 4 * u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_ptr_t)(dK + gi * 512), 16, (int)koff[u], 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_ptr_t)(dV + gi * 512), 16, (int)voff[u], 0, 0, 0);
     }
   };
   // keys past the request's length on its last page: V^T columns zeroed in LDS
@@ -323,9 +348,11 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
       __syncthreads();
     }
   };
-  for (int p = 0; p < n_pages; p += 2) {
-    step(p, sK0, sV0, sK1, sV1);
-    if (p + 1 < n_pages) step(p + 1, sK1, sV1, sK0, sV0);
+  // one loop body for both buffers (the buffer offset is uniform), so the
+  // fragment addresses are not held twice
+  for (int p = 0; p < n_pages; ++p) {
+    const int b = (p & 1) * (64 * DH);
+    step(p, sK0 + b, sV0 + b, sK0 + (64 * DH - b), sV0 + (64 * DH - b));
   }
   // every step ends on a barrier, so no page buffer is read any more: waves
   // 0-1 park their output rows in sK0, waves 2-3 in sK1
