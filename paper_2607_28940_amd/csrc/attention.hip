@@ -135,10 +135,9 @@ __device__ __forceinline__ void mfma_attend_frags(KFrag kfrag, VFrag vfrag, cons
   for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
     for (int t = 0; t < 8; ++t) pf[ks][t] = (bf16)s[ks >> 1][8 * (ks & 1) + t];
-  // from LDS: the V^T fragment reads start after the softmax and run four
-  // ahead of their MFMAs, as the K reads do, instead of all being hoisted
-  // above the softmax (which holds 64 more registers through it)
-  if (FROM_LDS) __builtin_amdgcn_sched_barrier(0);
+  // from LDS: the V^T fragment reads run four ahead of their MFMAs, as the K
+  // reads do, instead of all sixteen being hoisted above the softmax (which
+  // would hold 64 more registers through it)
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
