@@ -348,15 +348,26 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
   const int srow = tid >> 3, sslot = tid & 7;
   const int wofs = srow * PK + ((sslot ^ ((srow >> 1) & 7)) << 3);
   bf16x8 ga[8], gb[8];
-  // rows past M read row M - 1 (their results are never distinct from it)
+  // Operands through raw buffer loads: the lane's byte offset within a tile is
+  // fixed (row srow + 32 u, slot sslot), the tile's row base is added as one
+  // 32-bit value and k0 travels in the scalar offset. Rows past M fall beyond
+  // the A resource's extent and read as zeros; their results are not stored.
+  // (extents in bytes: the launcher keeps M lda and N K below 2^31 elements;
+  // word 3 of the resource as CDNA wants it for raw loads)
+  const __amdgpu_buffer_rsrc_t ra =
+      __builtin_amdgcn_make_buffer_rsrc((void*)A, 0, (int)(2u * (uint32_t)M * (uint32_t)lda), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rb =
+      __builtin_amdgcn_make_buffer_rsrc((void*)Bt, 0, (int)(2u * (uint32_t)N * (uint32_t)K), 0x00020000);
+  const uint32_t la = 2u * (uint32_t)(srow * lda + sslot * 8), lb = 2u * (uint32_t)(srow * K + sslot * 8);
   auto gload = [&](auto Q_, int m0, int n0, int k0) {
     constexpr int Q = decltype(Q_)::value;
-    const int mlim = M - 1 - m0;
 #pragma unroll
     for (int v = 0; v < 2; ++v) {
       const int u = 2 * Q + v;
-      ga[u] = *reinterpret_cast<const bf16x8*>(A + (m0 + min(srow + 32 * u, mlim)) * lda + sslot * 8 + k0);
-      gb[u] = *reinterpret_cast<const bf16x8*>(Bt + (n0 + srow + 32 * u) * K + sslot * 8 + k0);
+      const uint32_t oa = 2u * ((uint32_t)(m0 + 32 * u) * (uint32_t)lda) + la;
+      const uint32_t ob = 2u * ((uint32_t)(n0 + 32 * u) * (uint32_t)K) + lb;
+      ga[u] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(ra, (int)oa, 2 * k0, 0));
+      gb[u] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rb, (int)ob, 2 * k0, 0));
     }
   };
   auto lstore = [&](auto Q_, int stage) {
@@ -502,7 +513,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
     // (16-byte unit q of row r at unit q ^ (r % 16): conflict-free both ways)
     // and reads them back row-contiguously, 8 lanes per 128-byte row segment;
     // bias, GELU or residual applied with one rounding to bf16. Rows past M
-    // rewrite row M - 1 with its own values.
+    // (computed from zero rows) are not stored.
     floatx4 bv[2][2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -542,7 +553,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
           const int r = er + 8 * u;
           const floatx4 x0 = *reinterpret_cast<const floatx4*>(park + r * 64 + (((2 * ec) ^ (r & 15)) << 2));
           const floatx4 x1 = *reinterpret_cast<const floatx4*>(park + r * 64 + (((2 * ec + 1) ^ (r & 15)) << 2));
-          const int m = min(cm0 + wm * 128 + j * 32 + r, M - 1);
+          const int m = cm0 + wm * 128 + j * 32 + r;
           bf16x8 o;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
@@ -551,7 +562,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
             o[e] = (bf16)epilogue<EPI>(x0[e], bv[h][0][e], r0);
             o[e + 4] = (bf16)epilogue<EPI>(x1[e], bv[h][1][e], r1);
           }
-          *reinterpret_cast<bf16x8*>(C + (size_t)m * ldc + cn0 + wn * 128 + 64 * h + ec * 8) = o;
+          if (m < M) *reinterpret_cast<bf16x8*>(C + (size_t)m * ldc + cn0 + wn * 128 + 64 * h + ec * 8) = o;
         }
       }
   }
@@ -639,13 +650,12 @@ hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const fl
   // runs three k steps ahead), element offsets within int32.
   if (N % PT == 0 && K % (2 * PK) == 0 && K >= 4 * PK && M >= 2048 && (long long)M * lda < (1ll << 31) &&
       (long long)N * K < (1ll << 31)) {
-    static int n_cu = 0;
-    if (n_cu <= 0) {
-      int dev = 0;
-      if (hipGetDevice(&dev) != hipSuccess ||
-          hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 8)
-        n_cu = 256;
-    }
+    // the current device's CU count (a host-side property lookup, per call so
+    // that threads driving different devices never share it)
+    int n_cu = 0, dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 8)
+      n_cu = 256;
     const int tiles_n = N / PT, tiles_m = (M + PT - 1) / PT, n_tiles = tiles_n * tiles_m;
     const int per_xcd = (n_tiles + 7) / 8;
     const int grid = 8 * std::max(1, std::min(n_cu / 8, per_xcd));
