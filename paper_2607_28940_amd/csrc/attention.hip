@@ -68,10 +68,22 @@ __device__ __forceinline__ int v_frag(int row, int slot) {
 // kfrag(kb, kk) is K row kb * 32 + l32, features 16 kk + 8 hi .. + 7;
 // vfrag(ks, db) is V^T row 32 db + l32, stored columns
 // 32 (ks / 2) + 16 (ks % 2) + 8 hi .. + 7. FROM_LDS adds scheduling hints
-// for fragments read from LDS.
-template <int DH, bool FROM_LDS, class KFrag, class VFrag, class Mask>
-__device__ __forceinline__ void mfma_attend_frags(KFrag kfrag, VFrag vfrag, const bf16x8 (&qf)[DH / 16],
-                                                  MfmaAcc<DH>& acc, float scale_log2, int hi, bool masked, Mask mask) {
+// for fragments read from LDS (each read four ahead of the MFMA that uses it).
+template <int N>  // N fragment reads for N MFMAs
+__device__ __forceinline__ void pace_lds_reads() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+  for (int g = 0; g < N - 4; ++g) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+}
+
+// First half: S^T = K Q^T, the online softmax update and P^T in bf16.
+template <int DH, bool FROM_LDS, class KFrag, class Mask>
+__device__ __forceinline__ void mfma_qk_softmax(KFrag kfrag, const bf16x8 (&qf)[DH / 16], MfmaAcc<DH>& acc,
+                                                float scale_log2, int hi, bool masked, Mask mask, bf16x8 (&pf)[4]) {
   floatx16 s[2];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
@@ -80,16 +92,7 @@ __device__ __forceinline__ void mfma_attend_frags(KFrag kfrag, VFrag vfrag, cons
 #pragma unroll
     for (int kk = 0; kk < DH / 16; ++kk) s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kfrag(kb, kk), qf[kk], s[kb], 0, 0, 0);
   }
-  if (FROM_LDS) {
-    // keep four K fragment reads in flight ahead of the MFMA that uses them
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-    for (int g = 0; g < DH / 8 - 4; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-  }
+  if (FROM_LDS) pace_lds_reads<DH / 8>();
   if (masked) {  // wave-uniform
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -130,27 +133,30 @@ __device__ __forceinline__ void mfma_attend_frags(KFrag kfrag, VFrag vfrag, cons
     }
   rs = xor32_sum(rs);
   acc.l += rs;
-  bf16x8 pf[4];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
     for (int t = 0; t < 8; ++t) pf[ks][t] = (bf16)s[ks >> 1][8 * (ks & 1) + t];
-  // from LDS: the V^T fragment reads run four ahead of their MFMAs, as the K
-  // reads do, instead of all sixteen being hoisted above the softmax (which
-  // would hold 64 more registers through it)
+}
+
+// Second half: O^T += V^T P^T. From LDS the V^T fragment reads run four ahead
+// of their MFMAs, as the K reads do, instead of all sixteen being hoisted
+// above the softmax (which would hold 64 more registers through it).
+template <int DH, bool FROM_LDS, class VFrag>
+__device__ __forceinline__ void mfma_pv(VFrag vfrag, const bf16x8 (&pf)[4], MfmaAcc<DH>& acc) {
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
     for (int db = 0; db < DH / 32; ++db) acc.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(ks, db), pf[ks], acc.o[db], 0, 0, 0);
-  if (FROM_LDS) {
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-    for (int g = 0; g < DH / 8 - 4; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-  }
+  if (FROM_LDS) pace_lds_reads<DH / 8>();
+}
+
+template <int DH, bool FROM_LDS, class KFrag, class VFrag, class Mask>
+__device__ __forceinline__ void mfma_attend_frags(KFrag kfrag, VFrag vfrag, const bf16x8 (&qf)[DH / 16],
+                                                  MfmaAcc<DH>& acc, float scale_log2, int hi, bool masked, Mask mask) {
+  bf16x8 pf[4];
+  mfma_qk_softmax<DH, FROM_LDS>(kfrag, qf, acc, scale_log2, hi, masked, mask, pf);
+  mfma_pv<DH, FROM_LDS>(vfrag, pf, acc);
 }
 
 // The same tile with K and V^T staged in LDS.
@@ -203,6 +209,36 @@ __device__ __forceinline__ void mfma_store_out_staged(const MfmaAcc<DH>& acc, bf
     }
   }
 }
+
+// Direct HBM/L2 -> LDS copy of one page's 64 x DH K slab or DH x 64 V^T slab
+// by the four waves of a block: wave w moves the 1 KB pieces w, w + 4, ...;
+// lane l of a piece fills 16-byte LDS slot l with the chunk the XOR swizzle
+// puts there (K: row r, slot s holds chunk s ^ (r mod DH/8); V^T: slot s
+// holds chunk s ^ ((r / 2) mod 8)). Piece w + 4u lies 4u KB after piece w in
+// the slab and in LDS with the same swizzle, so one 32-bit lane offset per
+// slab and a scalar step serve every piece, and per page only the slab base
+// (scalar registers, in a raw buffer resource) changes.
+template <int DH>
+struct PageDma {
+  typedef __attribute__((address_space(3))) void* lds_ptr_t;
+  uint32_t koff, voff;  // bytes from the slab start to the lane's chunk of piece w
+  int piece0;           // element offset of piece w in LDS
+  __device__ __forceinline__ PageDma(int wave, int lane) {
+    const int e = wave * 512 + lane * 8;  // the lane's first element in piece w
+    const int kr = e / DH, ks = (e % DH) >> 3;
+    const int vr = e >> 6, vs = (e & 63) >> 3;
+    koff = 2u * (uint32_t)(kr * DH + ((ks ^ (kr & (DH / 8 - 1))) << 3));
+    voff = 2u * (uint32_t)(vr * 64 + ((vs ^ ((vr >> 1) & 7)) << 3));
+    piece0 = wave * 512;
+  }
+  __device__ __forceinline__ void load(const bf16* slab, uint32_t off, bf16* dst) const {
+    // word 3 of the resource as CDNA wants it for raw loads; extent = the slab
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc((void*)slab, 0, 128 * DH, 0x00020000);
+#pragma unroll
+    for (int u = 0; u < DH / 32; ++u)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(dst + piece0 + 2048 * u), 16, (int)off, 4096 * u, 0, 0);
+  }
+};
 
 // ============================================================================
 // bf16 paged attention on MFMA.
@@ -277,33 +313,13 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
   // Pages travel HBM/L2 -> LDS with buffer_load_dwordx4 ... lds: each wave
   // moves DH/32 KB of the K slab and as much of the V^T slab per page; lane l
   // of a 1 KB load fills 16-byte slot l of it with the chunk the swizzle puts
-  // there. The lanes' byte offsets within a slab are fixed, so they are
-  // computed once; per page only the slab bases (scalar) change. Page p+1 is
-  // requested while page p is used; every wave waits for its own loads before
-  // the page's closing barrier.
-  typedef __attribute__((address_space(3))) void* lds_ptr_t;
-  uint32_t koff[DH / 32], voff[DH / 32];
-#pragma unroll
-  for (int u = 0; u < DH / 32; ++u) {
-    const int e = (wave + 4 * u) * 512 + lane * 8;  // first element of the lane's chunk of 1 KB piece wave + 4u
-    const int kr = e / DH, ks = (e % DH) >> 3;
-    const int vr = e >> 6, vs = (e & 63) >> 3;
-    koff[u] = 2u * (uint32_t)(kr * DH + ((ks ^ (kr & (DH / 8 - 1))) << 3));
-    voff[u] = 2u * (uint32_t)(vr * 64 + ((vs ^ ((vr >> 1) & 7)) << 3));
-  }
+  // there. Page p+1 is requested while page p is used; every wave waits for
+  // its own loads before the page's closing barrier.
+  const PageDma<DH> pd(wave, lane);
   auto dma = [&](int p, bf16* dK, bf16* dV) {
     const bf16* base = pool + (size_t)ptab[p] * g.page_elems;
-    // raw buffer resources over the two 64 x DH slabs (word 3 as CDNA wants it)
-    const __amdgpu_buffer_rsrc_t kr =
-        __builtin_amdgcn_make_buffer_rsrc((void*)(base + g.k_off(layer_slot, h)), 0, 128 * DH, 0x00020000);
-    const __amdgpu_buffer_rsrc_t vr =
-        __builtin_amdgcn_make_buffer_rsrc((void*)(base + g.v_off(layer_slot, h)), 0, 128 * DH, 0x00020000);
-#pragma unroll
-    for (int u = 0; u < DH / 32; ++u) {
-      const int gi = wave + 4 * u;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_ptr_t)(dK + gi * 512), 16, (int)koff[u], 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_ptr_t)(dV + gi * 512), 16, (int)voff[u], 0, 0, 0);
-    }
+    pd.load(base + g.k_off(layer_slot, h), pd.koff, dK);
+    pd.load(base + g.v_off(layer_slot, h), pd.voff, dV);
   };
   // keys past the request's length on its last page: V^T columns zeroed in LDS
   // (the page may hold anything there; their K logits are masked anyway)
@@ -355,6 +371,109 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
   }
   // every step ends on a barrier, so no page buffer is read any more: waves
   // 0-1 park their output rows in sK0, waves 2-3 in sK1
+  mfma_store_out_staged<DH>(acc, (wave < 2 ? sK0 : sK1) + (wave & 1) * 32 * DH, out, ldo, h * DH, lane,
+                            tile.q_begin + wave * 32, tile.q_count - wave * 32, rq.qa_n, rq.qa_row, rq.qb_row);
+}
+
+// ============================================================================
+// The same cross-attention (no causal mask, d_h = 128) with three blocks per
+// CU, i.e. three waves per SIMD to overlap each wave's dependent page chain
+// (QK on MFMA, softmax on the VALU, PV on MFMA) with two others instead of
+// one: 48 KB of LDS (K double-buffered, V^T single-buffered) and at most 168
+// registers. Page p + 1's K is requested at the top of page p's body, page
+// p + 1's V^T once page p's PV has left the buffer; before the PV each wave
+// waits for its own V^T loads only (the K loads issued after them may stay in
+// flight) and the block meets at a barrier. Same arithmetic in the same order
+// as paged_attn_mfma, so the outputs are bitwise identical.
+// ============================================================================
+template <int DH>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) void paged_attn_mfma3(
+    const bf16* __restrict__ q, int ldq, bf16* __restrict__ out, int ldo, const bf16* __restrict__ pool,
+    const int32_t* __restrict__ page_table, int max_pages, PageGeom g, int layer_slot,
+    const AttnReq* __restrict__ reqs, const AttnTile* __restrict__ tiles, float scale_log2) {
+  constexpr int KLD = DH, VLD = 64;
+  // K page buffers 0, 1, then the V^T page buffer
+  __shared__ __attribute__((aligned(16))) bf16 sKV[3 * 64 * DH];
+  bf16* const sK0 = sKV;
+  bf16* const sK1 = sKV + 64 * DH;
+  bf16* const sV = sKV + 2 * 64 * DH;
+
+  const AttnTile tile = tiles[blockIdx.x];
+  if (tile.q_count <= 0) return;
+  const AttnReq rq = reqs[tile.req];
+  const int h = tile.head;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, hi = lane >> 5;
+  const bool wave_active = wave * 32 < tile.q_count;
+  const int i = tile.q_begin + min(wave * 32 + l32, tile.q_count - 1);
+  const int row = i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
+
+  bf16x8 qf[DH / 16];
+  {
+    const bf16* qr = q + (size_t)row * ldq + h * DH + 8 * hi;
+#pragma unroll
+    for (int kk = 0; kk < DH / 16; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qr + 16 * kk);
+  }
+  MfmaAcc<DH> acc;
+  acc.init();
+
+  const int kv_len = rq.kv_len;
+  const int n_pages = (kv_len + kPage - 1) / kPage;
+  const bool partial = kv_len % kPage != 0;
+  const int32_t* ptab = page_table + (size_t)rq.slot * max_pages;
+  const PageDma<DH> pd(wave, lane);
+  auto page = [&](int p) { return pool + (size_t)ptab[p] * g.page_elems; };
+  auto zero_tail = [&](int p) {
+    const int valid = kv_len - p * kPage;
+    for (int e = tid; e < DH * 64; e += 256) {
+      const int r = e >> 6, col = e & 63;
+      const int chunk = (col >> 3) ^ ((r >> 1) & 7);
+      if (vt_col(chunk * 8 + (col & 7)) >= valid) sV[e] = (bf16)0.f;
+    }
+  };
+  pd.load(page(0) + g.k_off(layer_slot, h), pd.koff, sK0);
+  pd.load(page(0) + g.v_off(layer_slot, h), pd.voff, sV);
+  __syncthreads();
+  if (n_pages == 1 && partial) {
+    zero_tail(0);
+    __syncthreads();
+  }
+  for (int p = 0; p < n_pages; ++p) {
+    const int b = (p & 1) * (64 * DH);
+    const bf16* cK = sK0 + b;
+    if (p + 1 < n_pages) pd.load(page(p + 1) + g.k_off(layer_slot, h), pd.koff, sK0 + (64 * DH - b));
+    const int key0 = p * kPage;
+    bf16x8 pf[4];
+    if (wave_active) {
+      auto kfrag = [&](int kb, int kk) {
+        return *reinterpret_cast<const bf16x8*>(&cK[k_frag<DH, KLD, true>(kb * 32 + l32, 2 * kk + hi)]);
+      };
+      mfma_qk_softmax<DH, true>(kfrag, qf, acc, scale_log2, hi, key0 + kPage > kv_len, [&](int kl, float x) {
+        return key0 + kl < kv_len ? x : -INFINITY;
+      }, pf);
+    }
+    if (p > 0) {
+      // V^T of page p (requested after page p - 1's PV) in LDS for every wave;
+      // the DH / 32 K loads of page p + 1 issued since may stay in flight
+      if (p + 1 < n_pages) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(DH / 32) : "memory");
+      else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+      if (p + 1 == n_pages && partial) {
+        zero_tail(p);
+        __syncthreads();
+      }
+    }
+    if (wave_active) {
+      auto vfrag = [&](int ks, int db) {
+        const int kbase = (ks >> 1) * 32 + 16 * (ks & 1) + 8 * hi;  // in the V^T tile's permuted key order
+        return *reinterpret_cast<const bf16x8*>(&sV[v_frag<VLD, true>(32 * db + l32, kbase >> 3)]);
+      };
+      mfma_pv<DH, true>(vfrag, pf, acc);
+    }
+    __syncthreads();  // K and V^T of page p no longer read; K of page p + 1 landed
+    if (p + 1 < n_pages) pd.load(page(p + 1) + g.v_off(layer_slot, h), pd.voff, sV);
+  }
+  // every body ends on a barrier and the last requests nothing: waves 0-1
+  // park their output rows in K buffer 0, waves 2-3 in K buffer 1
   mfma_store_out_staged<DH>(acc, (wave < 2 ? sK0 : sK1) + (wave & 1) * 32 * DH, out, ldo, h * DH, lane,
                             tile.q_begin + wave * 32, tile.q_count - wave * 32, rq.qa_n, rq.qa_row, rq.qb_row);
 }
@@ -760,7 +879,10 @@ hipError_t launch_paged_attention(bool bf, const void* q, int ldq, void* out, in
     if (g.dh == 64) {
       if (causal) TX_PA(64, true); else TX_PA(64, false);
     } else {
-      if (causal) TX_PA(128, true); else TX_PA(128, false);
+      if (causal) TX_PA(128, true);
+      else
+        paged_attn_mfma3<128><<<n_tiles, 256, 0, s>>>(qq, ldq, oo, ldo, pp, page_table, max_pages, g, layer_slot,
+                                                       reqs, tiles, sl2);
     }
 #undef TX_PA
     return hipGetLastError();

@@ -15,6 +15,8 @@
 // of the 8 XCDs (the hardware deals workgroup b to XCD b % 8) works through a
 // contiguous range of them, walked in groups of row blocks so that operand
 // blocks are reused from that XCD's L2.
+#include <atomic>
+
 #include "tx_internal.h"
 
 #include <algorithm>
@@ -650,12 +652,17 @@ hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const fl
   // runs three k steps ahead), element offsets within int32.
   if (N % PT == 0 && K % (2 * PK) == 0 && K >= 4 * PK && M >= 2048 && (long long)M * lda < (1ll << 31) &&
       (long long)N * K < (1ll << 31)) {
-    // the current device's CU count (a host-side property lookup, per call so
-    // that threads driving different devices never share it)
-    int n_cu = 0, dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 8)
-      n_cu = 256;
+    // the current device's CU count, looked up once per device
+    static std::atomic<int> cu_of_device[64];
+    int dev = 0, n_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = -1;
+    if (dev >= 0) n_cu = cu_of_device[dev].load(std::memory_order_relaxed);
+    if (n_cu <= 0) {
+      if (dev < 0 || hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+          n_cu < 8)
+        n_cu = 256;
+      if (dev >= 0) cu_of_device[dev].store(n_cu, std::memory_order_relaxed);
+    }
     const int tiles_n = N / PT, tiles_m = (M + PT - 1) / PT, n_tiles = tiles_n * tiles_m;
     const int per_xcd = (n_tiles + 7) / 8;
     const int grid = 8 * std::max(1, std::min(n_cu / 8, per_xcd));
