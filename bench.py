@@ -16,8 +16,10 @@ resident in HBM when it starts. Prints one JSON line.
                                       # each against its own prefix of the cache
 
 The JSON carries the roofline of the dominant kernel, whose per-launch time
-comes from HIP events the library records around each launch on the stream
-(tx_profile_*), and the fp64 CPU oracle's own throughput on a bounded sample.
+comes from HIP events the library records around its launches on the stream
+during the timed steps (tx_profile_*: a few untimed steps with every launch
+bracketed pick that kernel and give the per-class table first), and the fp64
+CPU oracle's own throughput on a bounded sample.
 """
 from __future__ import annotations
 
@@ -149,6 +151,8 @@ def main():
                          "every user's cache (through the causal encoder, in place), then scores")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-launch events")
+    ap.add_argument("--profile-steps", type=int, default=3,
+                    help="untimed steps with every launch bracketed by events (per-class table)")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="HBM bytes per launch from rocprofv3 counters (optional)")
     ap.add_argument("--calib-copy", action="store_true",
@@ -183,7 +187,8 @@ def main():
     if args.append and (wl.n_append <= 0 or args.events):
         print("--append needs a workload with appended events (--workload append) and no --events", file=sys.stderr)
         sys.exit(2)
-    grow = wl.n_append * (args.warmup + args.steps) if args.append else 0  # tokens appended per user
+    extra = 0 if args.no_profile else args.profile_steps  # untimed profiled steps
+    grow = wl.n_append * (args.warmup + extra + args.steps) if args.append else 0  # tokens appended per user
     n_pages = sum((wl.L[u] + grow + 63) // 64 for u in users)
     cache = T.KVCache(model, n_pages=n_pages, max_requests=n_users, max_tokens=max(wl.L) + grow)
     # build every user's cache (untimed), a few at a time
@@ -237,8 +242,18 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    prof_all, dom = {}, None
     if not args.no_profile:
+        # per-class launch times from untimed profiled steps; the timed steps
+        # then bracket only the dominant class's launches with event pairs
         T.profile_enable(True)
+        for _ in range(args.profile_steps):
+            step()
+        torch.cuda.synchronize()
+        prof_all = T.profile_read()
+        dom = max(prof_all, key=lambda k: prof_all[k]["ms"])
+        T.profile_enable(True)
+        T.profile_select([dom])
     stream = torch.cuda.current_stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -255,7 +270,7 @@ def main():
     assert bool(torch.isfinite(out).all()), "non-finite scores"
 
     if args.append:  # cached length grows by n_append per step; the work model takes the timed average
-        avg_len = [L + wl.n_append * (args.warmup + (args.steps + 1) / 2) for L in wl.L]
+        avg_len = [L + wl.n_append * (args.warmup + extra + (args.steps + 1) / 2) for L in wl.L]
         work = score_work(dataclasses.replace(wl, L=[int(round(x)) for x in avg_len]))
     else:
         work = score_work(wl)
@@ -265,20 +280,23 @@ def main():
     peak = PEAK_BF16_TFLOPS if m.dtype == "bf16" else PEAK_FP32_TFLOPS
 
     kernels = {}
-    for name, p in prof.items():
+    for name, p in prof_all.items():
         avg = p["ms"] / p["launches"]
-        kernels[name] = {"avg_ms": round(avg, 5), "launches_per_step": p["launches"] / args.steps,
-                         "share": round(p["ms"] / (ms * args.steps), 4),
+        kernels[name] = {"avg_ms": round(avg, 5), "launches_per_step": p["launches"] / args.profile_steps,
+                         "share": round(p["ms"] / (ms * args.profile_steps), 4),
                          "tflops": round(p["flops"] / (p["ms"] / 1e3) / 1e12, 2) if p["flops"] else None,
                          "gbs": round(p["bytes"] / (p["ms"] / 1e3) / 1e9, 1)}
     roofline = None
-    if prof:
-        dom = max(prof, key=lambda k: prof[k]["ms"])
+    if prof.get(dom, {}).get("launches"):
         p = prof[dom]
         avg_s = p["ms"] / p["launches"] / 1e3
         fl_launch, by_launch = p["flops"] / p["launches"], p["bytes"] / p["launches"]
         mfma = fl_launch > 0 and fl_launch / max(by_launch, 1) > peak * 1e12 / (PEAK_HBM_GBS * 1e9)
-        traffic = measured_traffic(args.traffic_json, dom)
+        # the counters were taken on the default headline run: other
+        # workloads and modes launch the same kernel on other shapes
+        default_run = (args.workload == "headline" and not args.append and not args.events and not args.actions
+                       and not args.l_local)
+        traffic = measured_traffic(args.traffic_json, dom) if default_run else None
         if mfma:
             ach = fl_launch / avg_s / 1e12
             roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",

@@ -257,6 +257,11 @@ int score_events(const tx_kv_cache* cache, int32_t n_events, const int32_t* req_
  * of that launch (the work the method defines for it, not what the kernel
  * happens to move). tx_profile_enable clears earlier records. */
 int tx_profile_enable(int32_t on);
+/* Restricts recording to the classes whose bit (1 << class index) is set in
+ * class_mask, so that a timed region carries event pairs only around the
+ * launches it reports; tx_profile_enable resets it to every class. Always
+ * TX_OK (bits past tx_profile_classes() are ignored). */
+int tx_profile_select(uint64_t class_mask);
 int32_t tx_profile_classes(void);
 const char* tx_profile_class_name(int32_t i);
 /* Per class (arrays of tx_profile_classes() entries, any may be NULL): summed

@@ -509,6 +509,7 @@ const char* const kClassNames[K_COUNT] = {
 // enabled; totals are folded in when read.
 struct Profiler {
   bool on = false;
+  uint64_t mask = ~0ull;  // classes recorded while on
   struct Rec {
     int cls;
     hipEvent_t a, b;
@@ -563,7 +564,7 @@ struct ProfScope {
   double fl, by;
   hipEvent_t a = nullptr;
   ProfScope(int c, hipStream_t s, double f, double b) : cls(c), st(s), fl(f), by(b) {
-    if (g_prof.on && (a = g_prof.get())) (void)hipEventRecord(a, st);
+    if (g_prof.on && ((g_prof.mask >> c) & 1) && (a = g_prof.get())) (void)hipEventRecord(a, st);
   }
   ~ProfScope() {
     if (!a) return;
@@ -586,6 +587,12 @@ extern "C" {
 int tx_profile_enable(int32_t on) {
   g_prof.clear();
   g_prof.on = on != 0;
+  g_prof.mask = ~0ull;
+  return TX_OK;
+}
+
+int tx_profile_select(uint64_t class_mask) {
+  g_prof.mask = class_mask;
   return TX_OK;
 }
 

@@ -79,6 +79,7 @@ _SIGS = {
     "score_candidates": (ctypes.c_int, [VP, ctypes.c_int32, I32P, VP, I64P, VP, I64P, VP, VP, ctypes.c_size_t, VP]),
     "score_events": (ctypes.c_int, [VP, ctypes.c_int32, I32P, I64P, VP, I64P, VP, I64P, VP, VP, ctypes.c_size_t, VP]),
     "tx_profile_enable": (ctypes.c_int, [ctypes.c_int32]),
+    "tx_profile_select": (ctypes.c_int, [ctypes.c_uint64]),
     "tx_profile_classes": (ctypes.c_int32, []),
     "tx_profile_class_name": (ctypes.c_char_p, [ctypes.c_int32]),
     "tx_profile_read": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), I64P, ctypes.POINTER(ctypes.c_double),
@@ -291,6 +292,16 @@ class KVCache:
 
 def profile_enable(on: bool = True):
     check(lib().tx_profile_enable(1 if on else 0))
+
+
+def profile_select(classes) -> None:
+    """Record only the named kernel classes (until profile_enable)."""
+    L = lib()
+    names = [L.tx_profile_class_name(i).decode() for i in range(L.tx_profile_classes())]
+    mask = 0
+    for c in classes:
+        mask |= 1 << names.index(c)
+    check(L.tx_profile_select(mask))
 
 
 def profile_read() -> dict:
