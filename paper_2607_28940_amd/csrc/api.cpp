@@ -711,11 +711,13 @@ int check_ids(const tx_kv_cache* c, int n, const int32_t* ids) {
   return TX_OK;
 }
 
-// Per-row activation bytes of each operation.
+// Per-row activation bytes of each operation: the model-type buffers, two
+// pre-LN sum buffers (the sum type has the model type's width) and two
+// LayerNorm row-statistics records.
 size_t row_bytes(const tx_model* m, int op) {
   const size_t d = m->d, F = m->F;
-  if (op == TX_OP_SCORE) return m->esz * (d + 3 * d + d + d + d + F);
-  return m->esz * (d + 3 * d + d + d + std::max(F, (size_t)(2 * m->n_dec) * d));
+  if (op == TX_OP_SCORE) return m->esz * (d + 3 * d + d + d + 2 * d + F) + 2 * sizeof(LnRow);
+  return m->esz * (d + 3 * d + d + 2 * d + std::max(F, (size_t)(2 * m->n_dec) * d)) + 2 * sizeof(LnRow);
 }
 
 // Workspace of the global-token pooling in an encoder pass: chunk partial
@@ -728,7 +730,7 @@ size_t pool_pass_bytes(const tx_model* m, int op, int n, int64_t rows) {
 }
 
 size_t pass_bytes(const tx_model* m, int op, int n, int64_t rows, int64_t max_rows) {
-  return meta_bound(n, rows, max_rows, m->H) + align_up(rows * row_bytes(m, op)) + 6 * 256 +
+  return meta_bound(n, rows, max_rows, m->H) + align_up(rows * row_bytes(m, op)) + 10 * 256 +
          pool_pass_bytes(m, op, n, rows);
 }
 
@@ -849,7 +851,10 @@ int run_encoder_pass(tx_kv_cache* c, const char* X, int64_t rows, const std::vec
   char* T = cv.take<char*>(rows * d * es);
   char* QKV = cv.take<char*>(rows * 3 * d * es);
   char* A = cv.take<char*>(rows * d * es);
-  char* Y = cv.take<char*>(rows * d * es);
+  // pre-LN sums and LayerNorm row statistics, alternating between sublayers:
+  // sublayer k writes Ys[k % 2] and adds LN(Ys[(k - 1) % 2]) as its residual
+  char* Ys[2] = {cv.take<char*>(rows * d * es), cv.take<char*>(rows * d * es)};
+  LnRow* Ss[2] = {cv.take<LnRow*>(rows * sizeof(LnRow)), cv.take<LnRow*>(rows * sizeof(LnRow))};
   char* Hf = cv.take<char*>(rows * std::max(F, 2 * m->n_dec * d) * es);
   float* pool_part = nullptr;
   char *gtok = nullptr, *gkv_rows = nullptr;
@@ -866,9 +871,12 @@ int run_encoder_pass(tx_kv_cache* c, const char* X, int64_t rows, const std::vec
     kv_bytes += (double)r.kv_len * 2 * d * es;
   }
   auto gemm_fb = [&](double N, double K) { return std::make_pair(2 * Md * N * K, esd * (Md * K + N * K + Md * N)); };
+  const float eps = m->cfg.ln_eps;
   for (int e = 0; e < m->n_enc; ++e) {
     const EncLayer& L = m->enc[e];
     const char* in = e == 0 ? X : T;
+    char *Y0 = Ys[0], *Y1 = Ys[1];  // sublayers 2e (attention) and 2e + 1 (FFN)
+    LnRow *S0 = Ss[0], *S1 = Ss[1];
     auto g1 = gemm_fb(3 * dd, dd), g2 = gemm_fb(dd, dd), g3 = gemm_fb(F, dd), g4 = gemm_fb(dd, F);
     TX_LAUNCH(K_ENC_GEMM, g1.first, g1.second,
               launch_gemm(bf, in, d, L.qkv.w, L.qkv.b, nullptr, 0, QKV, 3 * d, M, 3 * d, d, EPI_BIAS, st));
@@ -878,16 +886,19 @@ int run_encoder_pass(tx_kv_cache* c, const char* X, int64_t rows, const std::vec
     TX_LAUNCH(K_ENC_ATTN, 4 * dd * attn_pairs, kv_bytes + 2 * Md * dd * esd,
               launch_paged_attention(bf, QKV, 3 * d, A, d, c->pool, c->d_table, c->max_pages, c->geom, e, d_areq,
                                      d_tiles, (int)tiles.size(), true, L.rel, m->R, qb, st));
+    // residual: the input tokens (first layer) or the previous layer's output
+    // LN2(Y1), recomputed from its pre-LN sum
     TX_LAUNCH(K_ENC_GEMM, g2.first, g2.second + Md * dd * esd,
-              launch_gemm(bf, A, d, L.o.w, L.o.b, in, d, Y, d, M, d, d, EPI_BIAS_RESID, st));
-    TX_LAUNCH(K_ENC_LAYERNORM, 0, 2 * Md * dd * esd,
-              launch_layernorm(bf, Y, T, L.ln1g, L.ln1b, M, d, m->cfg.ln_eps, st));
+              e == 0 ? launch_gemm(bf, A, d, L.o.w, L.o.b, X, d, Y0, d, M, d, d, EPI_BIAS_RESID, st)
+                     : launch_gemm(bf, A, d, L.o.w, L.o.b, Y1, d, Y0, d, M, d, d, EPI_BIAS_RESLN, st,
+                                   LnResid{S1, m->enc[e - 1].ln2g, m->enc[e - 1].ln2b}));
+    TX_LAUNCH(K_ENC_LAYERNORM, 0, 2 * Md * dd * esd, launch_layernorm(bf, Y0, T, S0, L.ln1g, L.ln1b, M, d, eps, st));
     TX_LAUNCH(K_ENC_GEMM, g3.first, g3.second,
               launch_gemm(bf, T, d, L.f1.w, L.f1.b, nullptr, 0, Hf, F, M, F, d, EPI_BIAS_GELU, st));
     TX_LAUNCH(K_ENC_GEMM, g4.first, g4.second + Md * dd * esd,
-              launch_gemm(bf, Hf, F, L.f2.w, L.f2.b, T, d, Y, d, M, d, F, EPI_BIAS_RESID, st));
-    TX_LAUNCH(K_ENC_LAYERNORM, 0, 2 * Md * dd * esd,
-              launch_layernorm(bf, Y, T, L.ln2g, L.ln2b, M, d, m->cfg.ln_eps, st));
+              launch_gemm(bf, Hf, F, L.f2.w, L.f2.b, Y0, d, Y1, d, M, d, F, EPI_BIAS_RESLN, st,
+                          LnResid{S0, L.ln1g, L.ln1b}));
+    TX_LAUNCH(K_ENC_LAYERNORM, 0, 2 * Md * dd * esd, launch_layernorm(bf, Y1, T, S1, L.ln2g, L.ln2b, M, d, eps, st));
   }
   const int nkv = 2 * d * m->n_dec;
   auto g5 = gemm_fb(nkv, dd);
@@ -1088,7 +1099,10 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
   char* QKV = cv.take<char*>(M64 * 3 * d * es);
   char* A = cv.take<char*>(M64 * d * es);
   char* O = cv.take<char*>(M64 * d * es);
-  char* Y = cv.take<char*>(M64 * d * es);
+  // pre-LN sums and LayerNorm row statistics, alternating between sublayers:
+  // sublayer k writes Ys[k % 2] and adds LN(Ys[(k - 1) % 2]) as its residual
+  char* Ys[2] = {cv.take<char*>(M64 * d * es), cv.take<char*>(M64 * d * es)};
+  LnRow* Ss[2] = {cv.take<LnRow*>(M64 * sizeof(LnRow)), cv.take<LnRow*>(M64 * sizeof(LnRow))};
   char* Hf = cv.take<char*>(M64 * F * es);
   // The first layer reads the serving and candidate tokens where they are
   // (its QKV GEMM and the self-attention output GEMM's residual run once per
@@ -1141,6 +1155,11 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
     };
     auto q = gf(Md, 3 * dd, dd, 0), o = gf(Mrd, dd, dd, 1), xq = gf(Mrd, dd, dd, 0), xo = gf(Mrd, dd, dd, 1),
          f1 = gf(Mrd, F, dd, 0), f2 = gf(Mrd, dd, F, 1);
+    // sublayers 3l (self-attention), 3l + 1 (cross-attention), 3l + 2 (FFN):
+    // pre-LN sum buffer and row statistics of sublayer k, rows from r0 on
+    auto Yk = [&](int k) { return Ys[k & 1] + ro; };
+    auto Sk = [&](int k) { return Ss[k & 1] + r0; };
+    const int k0 = 3 * l;
     // layer input rows r0 .. M - 1: T, or the token arrays in place (first layer)
     const bool in_place = l == 0 && direct;
     TX_LAUNCH(K_GEMM_QKV, q.first, q.second, [&]() -> hipError_t {
@@ -1152,16 +1171,23 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
     }());
     TX_LAUNCH(K_SELF_ATTN, 4 * dd * (last ? self_cand : self_full), esd * (3 * Md * dd + Mrd * dd),
               launch_self_attention(bf, QKV, d, H, A, (const SelfReq*)(ws + o_sreq), stl, n_st, last, st));
+    // residual: the layer input, i.e. the tokens (first layer) or the previous
+    // layer's output LN3, recomputed from its pre-LN sum
     TX_LAUNCH(K_GEMM_O, o.first, o.second, [&]() -> hipError_t {
-      if (!in_place) return launch_gemm(bf, A + ro, d, L.o.w, L.o.b, T + ro, d, Y + ro, d, Mr, d, d, EPI_BIAS_RESID, st);
+      if (l > 0)
+        return launch_gemm(bf, A + ro, d, L.o.w, L.o.b, Yk(k0 - 1), d, Yk(k0), d, Mr, d, d, EPI_BIAS_RESLN, st,
+                           LnResid{Sk(k0 - 1), m->dec[l - 1].ln3g, m->dec[l - 1].ln3b});
+      if (!in_place)
+        return launch_gemm(bf, A + ro, d, L.o.w, L.o.b, T + ro, d, Yk(k0), d, Mr, d, d, EPI_BIAS_RESID, st);
       const size_t cs = (size_t)Ms * d * es;  // candidate rows start here in A and Y
       if (r0 == 0) {
-        hipError_t e = launch_gemm(bf, A, d, L.o.w, L.o.b, Xs, d, Y, d, (int)Ms, d, d, EPI_BIAS_RESID, st);
+        hipError_t e = launch_gemm(bf, A, d, L.o.w, L.o.b, Xs, d, Ys[0], d, (int)Ms, d, d, EPI_BIAS_RESID, st);
         if (e != hipSuccess) return e;
       }
-      return launch_gemm(bf, A + cs, d, L.o.w, L.o.b, Xc, d, Y + cs, d, (int)Mc, d, d, EPI_BIAS_RESID, st);
+      return launch_gemm(bf, A + cs, d, L.o.w, L.o.b, Xc, d, Ys[0] + cs, d, (int)Mc, d, d, EPI_BIAS_RESID, st);
     }());
-    TX_LAUNCH(K_LAYERNORM, 0, 2 * Mrd * dd * esd, launch_layernorm(bf, Y + ro, T + ro, L.ln1g, L.ln1b, Mr, d, eps, st));
+    TX_LAUNCH(K_LAYERNORM, 0, 2 * Mrd * dd * esd,
+              launch_layernorm(bf, Yk(k0), T + ro, Sk(k0), L.ln1g, L.ln1b, Mr, d, eps, st));
     TX_LAUNCH(K_GEMM_XQ, xq.first, xq.second,
               launch_gemm(bf, T + ro, d, L.xq.w, L.xq.b, nullptr, 0, A + ro, d, Mr, d, d, EPI_BIAS, st));
     TX_LAUNCH(K_CROSS_ATTN, 4 * dd * (last ? pairs_cand : pairs_full), kvb + 2 * Mrd * dd * esd,
@@ -1171,23 +1197,25 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
                      : launch_paged_attention(bf, A, d, O, d, c->pool, c->d_table, c->max_pages, c->geom,
                                               m->n_enc + l, areq, at, n_at, false, nullptr, 0, qb, st));
     TX_LAUNCH(K_GEMM_XO, xo.first, xo.second,
-              launch_gemm(bf, O + ro, d, L.xo.w, L.xo.b, T + ro, d, Y + ro, d, Mr, d, d, EPI_BIAS_RESID, st));
-    TX_LAUNCH(K_LAYERNORM, 0, 2 * Mrd * dd * esd, launch_layernorm(bf, Y + ro, T + ro, L.ln2g, L.ln2b, Mr, d, eps, st));
+              launch_gemm(bf, O + ro, d, L.xo.w, L.xo.b, Yk(k0), d, Yk(k0 + 1), d, Mr, d, d, EPI_BIAS_RESLN, st,
+                          LnResid{Sk(k0), L.ln1g, L.ln1b}));
+    TX_LAUNCH(K_LAYERNORM, 0, 2 * Mrd * dd * esd,
+              launch_layernorm(bf, Yk(k0 + 1), T + ro, Sk(k0 + 1), L.ln2g, L.ln2b, Mr, d, eps, st));
     TX_LAUNCH(K_GEMM_FFN1, f1.first, f1.second,
               launch_gemm(bf, T + ro, d, L.f1.w, L.f1.b, nullptr, 0, Hf + (size_t)r0 * F * es, F, Mr, F, d,
                           EPI_BIAS_GELU, st));
     TX_LAUNCH(K_GEMM_FFN2, f2.first, f2.second,
-              launch_gemm(bf, Hf + (size_t)r0 * F * es, F, L.f2.w, L.f2.b, T + ro, d, Y + ro, d, Mr, d, F,
-                          EPI_BIAS_RESID, st));
+              launch_gemm(bf, Hf + (size_t)r0 * F * es, F, L.f2.w, L.f2.b, Yk(k0 + 1), d, Yk(k0 + 2), d, Mr, d, F,
+                          EPI_BIAS_RESLN, st, LnResid{Sk(k0 + 1), L.ln2g, L.ln2b}));
     if (last) {
       const int k = std::max(1, m->n_act);
       TX_LAUNCH(K_LN_SCORE, 2 * Mrd * dd * k, Mrd * dd * esd + 4 * Mrd * k,
-                launch_layernorm_score(bf, Y + ro, L.ln3g, L.ln3b, m->ws, m->bs, scores + (size_t)co[a] * k, Mr, d,
-                                       eps, m->n_act, st));
+                launch_layernorm_score(bf, Yk(k0 + 2), L.ln3g, L.ln3b, m->ws, m->bs, scores + (size_t)co[a] * k, Mr,
+                                       d, eps, m->n_act, st));
     }
     else
       TX_LAUNCH(K_LAYERNORM, 0, 2 * Mrd * dd * esd,
-                launch_layernorm(bf, Y + ro, T + ro, L.ln3g, L.ln3b, Mr, d, eps, st));
+                launch_layernorm(bf, Yk(k0 + 2), T + ro, Sk(k0 + 2), L.ln3g, L.ln3b, Mr, d, eps, st));
   }
   return TX_OK;
 }

@@ -3,7 +3,11 @@
 // A is the packed activation matrix [M][K] (token rows), Bt the repacked weight
 // [N][K] (the layer's W [K][N] transposed so that both operands are contiguous
 // along K). Epilogues: +bias, +bias then exact-erf GELU (FFN), +bias + residual
-// (post-LN sublayers add the block input before LayerNorm, Sec. 4.1.2).
+// (post-LN sublayers add the block input before LayerNorm, Sec. 4.1.2). A
+// residual that is itself a LayerNorm output is recomputed in fp32 from the
+// stored pre-LN sum and its row statistics, so the residual stream never
+// passes through the rounded bf16 copy the sublayer used as its operand, and
+// the new pre-LN sum is stored in fp16 (see EPI_BIAS_RESLN).
 //
 // bf16 path: v_mfma_f32_32x32x16_bf16 with fp32 accumulation. The weight tile
 // is the MFMA "A" operand and the activation tile the "B" operand, so each
@@ -50,10 +54,36 @@ __device__ __forceinline__ float gelu_erf(float x) {
 
 template <int EPI>
 __device__ __forceinline__ float epilogue(float acc, float bias, float resid) {
+#pragma clang fp contract(off)
   float v = acc + bias;
   if (EPI == EPI_BIAS_GELU) v = gelu_erf(v);
-  if (EPI == EPI_BIAS_RESID) v += resid;
+  if (EPI >= EPI_BIAS_RESID) v += resid;
   return v;
+}
+
+// Residual element e of a 16-byte piece of R: the model-type value itself
+// (EPI_BIAS_RESID) or the LayerNorm of the fp16 pre-LN sum with row
+// statistics st and the column's gain g (EPI_BIAS_RESLN), whose offset every
+// kernel adds to the bias instead: (acc + (bias + b)) + (y * x + y') * g, the
+// same operations in the same order in each kernel, so that they agree
+// bitwise.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float ln_resid(float y, LnRow st, float g) {
+#pragma clang fp contract(off)
+  return fmaf(y, st.x, st.y) * g;
+}
+template <int EPI>
+__device__ __forceinline__ float resid8(const u32x4& raw, int e, LnRow st, float g) {
+  if (EPI == EPI_BIAS_RESID) return (float)__builtin_bit_cast(bf16x8, raw)[e];
+  if (EPI == EPI_BIAS_RESLN) return ln_resid((float)__builtin_bit_cast(f16x8, raw)[e], st, g);
+  return 0.f;
+}
+template <int EPI>
+__device__ __forceinline__ float resid4(const u32x2& raw, int e, LnRow st, float g) {
+  if (EPI == EPI_BIAS_RESID) return (float)__builtin_bit_cast(bf16x4, raw)[e];
+  if (EPI == EPI_BIAS_RESLN) return ln_resid((float)__builtin_bit_cast(f16x4, raw)[e], st, g);
+  return 0.f;
 }
 
 constexpr int GM = 128, GN = 128, GK = 64, GLD = GK + 8;
@@ -61,8 +91,9 @@ constexpr int GM = 128, GN = 128, GK = 64, GLD = GK + 8;
 template <int EPI>
 __global__ __launch_bounds__(256, 2) void gemm_bf16_mfma(const bf16* __restrict__ A, int lda,
                                                           const bf16* __restrict__ Bt, const float* __restrict__ bias,
-                                                          const bf16* __restrict__ R, int ldr, bf16* __restrict__ C,
-                                                          int ldc, int M, int N, int K, int tiles_n, int n_tiles) {
+                                                          const void* __restrict__ R, int ldr, void* __restrict__ C,
+                                                          int ldc, int M, int N, int K, int tiles_n, int n_tiles,
+                                                          LnResid ln) {
   __shared__ __attribute__((aligned(16))) bf16 sA[2][GM * GLD];
   __shared__ __attribute__((aligned(16))) bf16 sB[2][GN * GLD];
 
@@ -133,168 +164,39 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_mfma(const bf16* __restrict_
   for (int j = 0; j < 2; ++j) {
     const int m = m0 + wm * 64 + j * 32 + l32;
     if (m >= M) continue;
+    LnRow st{0.f, 0.f};
+    if (EPI == EPI_BIAS_RESLN) st = ln.stats[m];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int n = n0 + wn * 64 + i * 32 + 8 * g + 4 * hi;
-        const floatx4 b4 = *reinterpret_cast<const floatx4*>(bias + n);
-        float r4[4] = {0.f, 0.f, 0.f, 0.f};
-        if (EPI == EPI_BIAS_RESID) {
-          const bf16x4 rv = *reinterpret_cast<const bf16x4*>(R + (size_t)m * ldr + n);
+        floatx4 b4 = *reinterpret_cast<const floatx4*>(bias + n);
+        if (EPI >= EPI_BIAS_RESID) {
+          const u32x2 raw = *reinterpret_cast<const u32x2*>((const bf16*)R + (size_t)m * ldr + n);
+          floatx4 g4 = {0.f, 0.f, 0.f, 0.f};
+          if (EPI == EPI_BIAS_RESLN) {
+            g4 = *reinterpret_cast<const floatx4*>(ln.g + n);
+            b4 += *reinterpret_cast<const floatx4*>(ln.b + n);
+          }
+          f16x4 o;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) r4[q] = (float)rv[q];
+          for (int q = 0; q < 4; ++q)
+            o[q] = (f16)epilogue<EPI>(acc[i][j][4 * g + q], b4[q], resid4<EPI>(raw, q, st, g4[q]));
+          *reinterpret_cast<f16x4*>((f16*)C + (size_t)m * ldc + n) = o;
+        } else {
+          bf16x4 o;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) o[q] = (bf16)epilogue<EPI>(acc[i][j][4 * g + q], b4[q], 0.f);
+          *reinterpret_cast<bf16x4*>((bf16*)C + (size_t)m * ldc + n) = o;
         }
-        bf16x4 o;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = (bf16)epilogue<EPI>(acc[i][j][4 * g + q], b4[q], r4[q]);
-        *reinterpret_cast<bf16x4*>(C + (size_t)m * ldc + n) = o;
       }
     }
   }
 }
 
 
-// Large-tile kernel: 256x256 block tile, K step 64, 8 waves (2 per SIMD) as
-// 2x4, each wave 128 rows x 64 columns of C (2x4 MFMA tiles). Fragments of the
-// next 16-wide k step are read from LDS while the MFMAs of the current one run
-// (the scheduling barriers keep the compiler from sinking those reads next to
-// their use). The epilogue goes through LDS: each wave parks 32 rows x 64
-// columns of fp32 results in its own slice of the (then idle) tile buffers and
-// reads them back row-contiguously, so every global store writes 16 bytes per
-// lane and 8 lanes fill one 128-byte row segment; bias, GELU and residual are
-// applied in that phase, with a single rounding to bf16.
-constexpr int BM = 256, BN = 256, BK = 64, BLD = BK + 8, kGroupM = 8;
-
-template <int EPI>
-__global__ __launch_bounds__(512, 1) void gemm_bf16_mfma_256(const bf16* __restrict__ A, int lda,
-                                                             const bf16* __restrict__ Bt,
-                                                             const float* __restrict__ bias,
-                                                             const bf16* __restrict__ R, int ldr,
-                                                             bf16* __restrict__ C, int ldc, int M, int N, int K,
-                                                             int tiles_m, int tiles_n, int n_tiles) {
-  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * BLD];
-  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * BLD];
-
-  const int per_xcd = (n_tiles + 7) >> 3;
-  const int t = (int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3);
-  if (t >= n_tiles) return;
-  // grouped order: kGroupM row blocks share each column block in turn
-  const int group = t / (kGroupM * tiles_n);
-  const int first_m = group * kGroupM;
-  const int gm_size = min(tiles_m - first_m, kGroupM);
-  const int tm = first_m + (t % (kGroupM * tiles_n)) % gm_size;
-  const int tn = (t % (kGroupM * tiles_n)) / gm_size;
-  const int m0 = tm * BM, n0 = tn * BN;
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
-  const int l32 = lane & 31, hi = lane >> 5;
-
-  bf16x8 ra[4], rb[4];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int c = tid + 512 * u, r = c >> 3, col = (c & 7) * 8;
-      const int gm = min(m0 + r, M - 1);
-      ra[u] = *reinterpret_cast<const bf16x8*>(A + (size_t)gm * lda + k0 + col);
-      rb[u] = *reinterpret_cast<const bf16x8*>(Bt + (size_t)(n0 + r) * K + k0 + col);
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int c = tid + 512 * u, r = c >> 3, col = (c & 7) * 8;
-      *reinterpret_cast<bf16x8*>(&sA[buf][r * BLD + col]) = ra[u];
-      *reinterpret_cast<bf16x8*>(&sB[buf][r * BLD + col]) = rb[u];
-    }
-  };
-
-  floatx16 acc[2][4];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
-  const int nk = K / BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
-    bf16x8 fw[2][2], fx[2][4];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      fw[0][i] = *reinterpret_cast<const bf16x8*>(&sB[cur][(wn * 64 + i * 32 + l32) * BLD + hi * 8]);
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      fx[0][j] = *reinterpret_cast<const bf16x8*>(&sA[cur][(wm * 128 + j * 32 + l32) * BLD + hi * 8]);
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int f = ks & 1;
-      if (ks + 1 < BK / 16) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-          fw[f ^ 1][i] =
-              *reinterpret_cast<const bf16x8*>(&sB[cur][(wn * 64 + i * 32 + l32) * BLD + (ks + 1) * 16 + hi * 8]);
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          fx[f ^ 1][j] =
-              *reinterpret_cast<const bf16x8*>(&sA[cur][(wm * 128 + j * 32 + l32) * BLD + (ks + 1) * 16 + hi * 8]);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[f][i], fx[f][j], acc[i][j], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if (kt + 1 < nk) lstore(cur ^ 1);
-    __syncthreads();
-  }
-
-  // accumulator (i, j), element v: column wn*64 + i*32 + 8*(v/4) + 4*hi + v%4,
-  // row wm*128 + j*32 + l32 (within the block tile)
-  constexpr int ELD = 64 + 4;  // fp32 row stride of a wave's staging slice
-  float* stage = reinterpret_cast<float*>(&sA[0][0]) + wave * 32 * ELD;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const floatx4 v4 = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-        *reinterpret_cast<floatx4*>(stage + l32 * ELD + i * 32 + 8 * g + 4 * hi) = v4;
-      }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int q = lane + 64 * u, r = q >> 3, cc = (q & 7) * 8;
-      const int m = m0 + wm * 128 + j * 32 + r, n = n0 + wn * 64 + cc;
-      const floatx4 x0 = *reinterpret_cast<const floatx4*>(stage + r * ELD + cc);
-      const floatx4 x1 = *reinterpret_cast<const floatx4*>(stage + r * ELD + cc + 4);
-      if (m < M) {
-        const floatx4 b0 = *reinterpret_cast<const floatx4*>(bias + n);
-        const floatx4 b1 = *reinterpret_cast<const floatx4*>(bias + n + 4);
-        float rr[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-        if (EPI == EPI_BIAS_RESID) {
-          const bf16x8 rv = *reinterpret_cast<const bf16x8*>(R + (size_t)m * ldr + n);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) rr[e] = (float)rv[e];
-        }
-        bf16x8 o;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          o[e] = (bf16)epilogue<EPI>(x0[e], b0[e], rr[e]);
-          o[e + 4] = (bf16)epilogue<EPI>(x1[e], b1[e], rr[e + 4]);
-        }
-        *reinterpret_cast<bf16x8*>(C + (size_t)m * ldc + n) = o;
-      }
-    }
-  }
-}
+constexpr int kGroupM = 8;  // row blocks that share each column block in turn (L2 reuse)
 
 // Persistent four-wave kernel: one block per CU walks a run of 256x256 output
 // tiles. Four waves (one per SIMD) as 2x2, each wave 128x128 of C from 4x4
@@ -320,9 +222,9 @@ template <int EPI>
 __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ A, int lda,
                                                        const bf16* __restrict__ Bt,
                                                        const float* __restrict__ bias,
-                                                       const bf16* __restrict__ R, int ldr, bf16* __restrict__ C,
+                                                       const void* __restrict__ R, int ldr, void* __restrict__ C,
                                                        int ldc, int M, int N, int K, int tiles_m, int tiles_n,
-                                                       int n_tiles, int per_xcd) {
+                                                       int n_tiles, int per_xcd, LnResid ln) {
   __shared__ __attribute__((aligned(16))) bf16 lds[2 * kPStage];
   __shared__ __attribute__((aligned(16))) float park_all[4 * 32 * 64];
 
@@ -497,6 +399,19 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
 
   float* park = park_all + wave * 32 * 64;
   const int er = lane >> 3, ec = lane & 7;  // row (plus 8 u) and 8-float chunk of the read-back
+  // epilogue resources (extents in bytes, below 2^32: checked by the launcher)
+  // and the lane's fixed offsets: row wm * 128 + er (+ 32 j + 8 u), column
+  // wn * 128 + 8 ec (+ 64 h) of the tile; LayerNorm statistics of row wm * 128
+  // + l32 (+ 32 j)
+  const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)R, 0, EPI >= EPI_BIAS_RESID ? (int)(2u * (uint32_t)M * (uint32_t)ldr) : 0, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)ln.stats, 0, EPI == EPI_BIAS_RESLN ? (int)(8u * (uint32_t)M) : 0, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rc =
+      __builtin_amdgcn_make_buffer_rsrc(C, 0, (int)(2u * (uint32_t)M * (uint32_t)ldc), 0x00020000);
+  const uint32_t lr = 2u * (uint32_t)((wm * 128 + er) * ldr + wn * 128 + ec * 8);
+  const uint32_t lc = 2u * (uint32_t)((wm * 128 + er) * ldc + wn * 128 + ec * 8);
+  const uint32_t ls = 8u * (uint32_t)(wm * 128 + l32);
 
   for (int i = 0; i < my_tiles; ++i) {
     // the tile's first MFMAs take a zero accumulator input
@@ -514,21 +429,30 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
     // epilogue: per round each wave parks 32 rows x 64 columns of fp32 results
     // (16-byte unit q of row r at unit q ^ (r % 16): conflict-free both ways)
     // and reads them back row-contiguously, 8 lanes per 128-byte row segment;
-    // bias, GELU or residual applied with one rounding to bf16. Rows past M
-    // (computed from zero rows) are not stored.
-    floatx4 bv[2][2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      bv[h][0] = *reinterpret_cast<const floatx4*>(bias + cn0 + wn * 128 + 64 * h + ec * 8);
-      bv[h][1] = *reinterpret_cast<const floatx4*>(bias + cn0 + wn * 128 + 64 * h + ec * 8 + 4);
-    }
-    bf16x8 rres[4];
+    // bias, GELU or residual applied with one rounding (bf16, or fp16 for a
+    // pre-LN sum). Rows past M (computed from zero rows) are not stored.
+    // Rounds (j, h): 32 rows (32 j ..) x 64 columns (64 h ..) of the wave's
+    // 128 x 128. The residual pieces of a round are fetched one round ahead;
+    // the LayerNorm statistics of its rows (one row per lane l < 32, shared by
+    // both rounds of j) are handed to the lanes that need them by lane
+    // permutes. The column vectors (bias, and for a LayerNorm residual its gain
+    // and offset, the offset folded into the bias) are read again each round
+    // (L1 hits) rather than held through the epilogue. Residual, statistics
+    // and outputs go through raw buffer operations with 32-bit offsets: rows
+    // past M lie beyond the resources, read as zeros and are not written.
+    u32x4 rres[4];
+    LnRow stn{0.f, 0.f}, stc{0.f, 0.f};
     auto rload = [&](int j, int h) {
-      if (EPI == EPI_BIAS_RESID) {
+      if (EPI >= EPI_BIAS_RESID) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const int m = min(cm0 + wm * 128 + j * 32 + er + 8 * u, M - 1);
-          rres[u] = *reinterpret_cast<const bf16x8*>(R + (size_t)m * ldr + cn0 + wn * 128 + 64 * h + ec * 8);
+          const uint32_t o = 2u * ((uint32_t)(cm0 + j * 32 + 8 * u) * (uint32_t)ldr + (uint32_t)(cn0 + 64 * h)) + lr;
+          rres[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rr, (int)o, 0, 0));
+        }
+        if (EPI == EPI_BIAS_RESLN && h == 0) {
+          const uint32_t o = 8u * (uint32_t)(cm0 + j * 32) + ls;
+          const u32x2 v = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rs, (int)o, 0, 0));
+          stn = LnRow{__uint_as_float(v[0]), __uint_as_float(v[1])};
         }
       }
     };
@@ -546,25 +470,52 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
             const int q = ii * 8 + 2 * g + hi;
             *reinterpret_cast<floatx4*>(park + l32 * 64 + ((q ^ (l32 & 15)) << 2)) = v4;
           }
-        bf16x8 rcur[4];
+        u32x4 rcur[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) rcur[u] = rres[u];
+        if (h == 0) stc = stn;
         if (j * 2 + h + 1 < 8) rload((j * 2 + h + 1) >> 1, (j * 2 + h + 1) & 1);
+        asm volatile("" ::: "memory");  // keeps the column vectors from being held across rounds
+        const int ncol = cn0 + wn * 128 + 64 * h + ec * 8;
+        floatx4 cb[2], lg[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          cb[q] = *reinterpret_cast<const floatx4*>(bias + ncol + 4 * q);
+          if (EPI == EPI_BIAS_RESLN) {
+            cb[q] += *reinterpret_cast<const floatx4*>(ln.b + ncol + 4 * q);
+            lg[q] = *reinterpret_cast<const floatx4*>(ln.g + ncol + 4 * q);
+          }
+        }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int r = er + 8 * u;
           const floatx4 x0 = *reinterpret_cast<const floatx4*>(park + r * 64 + (((2 * ec) ^ (r & 15)) << 2));
           const floatx4 x1 = *reinterpret_cast<const floatx4*>(park + r * 64 + (((2 * ec + 1) ^ (r & 15)) << 2));
-          const int m = cm0 + wm * 128 + j * 32 + r;
-          bf16x8 o;
+          const uint32_t o_off = 2u * ((uint32_t)(cm0 + j * 32 + 8 * u) * (uint32_t)ldc + (uint32_t)(cn0 + 64 * h)) + lc;
+          u32x4 ov;
+          if (EPI >= EPI_BIAS_RESID) {
+            LnRow st{0.f, 0.f};
+            if (EPI == EPI_BIAS_RESLN) st = LnRow{__shfl(stc.x, r), __shfl(stc.y, r)};
+            f16x8 o;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float r0 = EPI == EPI_BIAS_RESID ? (float)rcur[u][e] : 0.f;
-            const float r1 = EPI == EPI_BIAS_RESID ? (float)rcur[u][e + 4] : 0.f;
-            o[e] = (bf16)epilogue<EPI>(x0[e], bv[h][0][e], r0);
-            o[e + 4] = (bf16)epilogue<EPI>(x1[e], bv[h][1][e], r1);
+            for (int e = 0; e < 4; ++e) {
+              const float r0 = resid8<EPI>(rcur[u], e, st, EPI == EPI_BIAS_RESLN ? lg[0][e] : 0.f);
+              const float r1 = resid8<EPI>(rcur[u], e + 4, st, EPI == EPI_BIAS_RESLN ? lg[1][e] : 0.f);
+              o[e] = (f16)epilogue<EPI>(x0[e], cb[0][e], r0);
+              o[e + 4] = (f16)epilogue<EPI>(x1[e], cb[1][e], r1);
+            }
+            ov = __builtin_bit_cast(u32x4, o);
+          } else {
+            bf16x8 o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              o[e] = (bf16)epilogue<EPI>(x0[e], cb[0][e], 0.f);
+              o[e + 4] = (bf16)epilogue<EPI>(x1[e], cb[1][e], 0.f);
+            }
+            ov = __builtin_bit_cast(u32x4, o);
           }
-          if (m < M) *reinterpret_cast<bf16x8*>(C + (size_t)m * ldc + cn0 + wn * 128 + 64 * h + ec * 8) = o;
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, ov),
+                                                 rc, (int)o_off, 0, 0);
         }
       }
   }
@@ -572,10 +523,18 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
 
 // Plain tiled GEMM for fp32 models and shapes the MFMA tiling does not cover:
 // 64x64 block tile, K step 16, each thread computes 4x4 outputs in fp32.
+// Sum type (pre-LN sums of the residual epilogues): fp16 beside bf16, fp32
+// beside fp32.
+template <typename T>
+using SumT = typename std::conditional<std::is_same<T, float>::value, float, f16>::type;
+
 template <typename T, int EPI>
 __global__ __launch_bounds__(256) void gemm_plain(const T* __restrict__ A, int lda, const T* __restrict__ Bt,
-                                                  const float* __restrict__ bias, const T* __restrict__ R, int ldr,
-                                                  T* __restrict__ C, int ldc, int M, int N, int K) {
+                                                  const float* __restrict__ bias, const void* __restrict__ R, int ldr,
+                                                  void* __restrict__ C, int ldc, int M, int N, int K, LnResid ln) {
+  typedef SumT<T> S;
+  typedef typename std::conditional<EPI == EPI_BIAS_RESLN, S, T>::type RT;  // residual element type
+  typedef typename std::conditional<(EPI >= EPI_BIAS_RESID), S, T>::type CT;  // output element type
   __shared__ float sA[16][64 + 4];
   __shared__ float sB[16][64 + 4];
   const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
@@ -605,53 +564,82 @@ __global__ __launch_bounds__(256) void gemm_plain(const T* __restrict__ A, int l
     }
     __syncthreads();
   }
+  const RT* Rt = (const RT*)R;
+  CT* Ct = (CT*)C;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int m = m0 + ty * 4 + i;
     if (m >= M) continue;
+    LnRow st{0.f, 0.f};
+    if (EPI == EPI_BIAS_RESLN) st = ln.stats[m];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int n = n0 + tx * 4 + j;
       if (n >= N) continue;
-      const float r = (EPI == EPI_BIAS_RESID) ? (float)R[(size_t)m * ldr + n] : 0.f;
-      C[(size_t)m * ldc + n] = (T)epilogue<EPI>(acc[i][j], bias[n], r);
+      float r = 0.f, bn = bias[n];
+      if (EPI == EPI_BIAS_RESID) r = (float)Rt[(size_t)m * ldr + n];
+      if (EPI == EPI_BIAS_RESLN) {
+        r = ln_resid((float)Rt[(size_t)m * ldr + n], st, ln.g[n]);
+        bn += ln.b[n];
+      }
+      Ct[(size_t)m * ldc + n] = (CT)epilogue<EPI>(acc[i][j], bn, r);
     }
   }
 }
 
 template <typename T>
 static hipError_t plain(const void* A, int lda, const void* Bt, const float* bias, const void* R, int ldr, void* C,
-                        int ldc, int M, int N, int K, Epilogue epi, hipStream_t s) {
+                        int ldc, int M, int N, int K, Epilogue epi, LnResid ln, hipStream_t s) {
   dim3 grid((N + 63) / 64, (M + 63) / 64);
   const T* a = (const T*)A;
   const T* b = (const T*)Bt;
-  const T* r = (const T*)R;
-  T* c = (T*)C;
+#define TX_PL(E) gemm_plain<T, E><<<grid, 256, 0, s>>>(a, lda, b, bias, R, ldr, C, ldc, M, N, K, ln)
   switch (epi) {
-    case EPI_BIAS: gemm_plain<T, EPI_BIAS><<<grid, 256, 0, s>>>(a, lda, b, bias, r, ldr, c, ldc, M, N, K); break;
-    case EPI_BIAS_GELU:
-      gemm_plain<T, EPI_BIAS_GELU><<<grid, 256, 0, s>>>(a, lda, b, bias, r, ldr, c, ldc, M, N, K);
-      break;
-    case EPI_BIAS_RESID:
-      gemm_plain<T, EPI_BIAS_RESID><<<grid, 256, 0, s>>>(a, lda, b, bias, r, ldr, c, ldc, M, N, K);
-      break;
+    case EPI_BIAS: TX_PL(EPI_BIAS); break;
+    case EPI_BIAS_GELU: TX_PL(EPI_BIAS_GELU); break;
+    case EPI_BIAS_RESID: TX_PL(EPI_BIAS_RESID); break;
+    case EPI_BIAS_RESLN: TX_PL(EPI_BIAS_RESLN); break;
   }
+#undef TX_PL
   return hipGetLastError();
 }
 
 hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const float* bias, const void* R, int ldr,
-                       void* C, int ldc, int M, int N, int K, Epilogue epi, hipStream_t s) {
+                       void* C, int ldc, int M, int N, int K, Epilogue epi, hipStream_t s, LnResid ln) {
   if (M <= 0) return hipSuccess;
-  if (!bf) return plain<float>(A, lda, Bt, bias, R, ldr, C, ldc, M, N, K, epi, s);
+  if (epi == EPI_BIAS_RESLN && (!ln.stats || !ln.g || !ln.b)) return hipErrorInvalidValue;
+  if (epi >= EPI_BIAS_RESID && !R) return hipErrorInvalidValue;
+  if (!bf) return plain<float>(A, lda, Bt, bias, R, ldr, C, ldc, M, N, K, epi, ln, s);
+  // The MFMA kernels address A, R and C with 32-bit byte offsets: a product
+  // whose operands span 2^31 elements or more runs as several row chunks.
+  {
+    const long long ld_max = std::max({(long long)lda, (long long)ldc, epi >= EPI_BIAS_RESID ? (long long)ldr : 1ll});
+    const long long rows_max = std::max(256ll, ((1ll << 31) - 1) / ld_max / 256 * 256);
+    if (M > rows_max) {
+      for (long long m0 = 0; m0 < M; m0 += rows_max) {
+        const int mc = (int)std::min(rows_max, (long long)M - m0);
+        LnResid lc = ln;
+        if (lc.stats) lc.stats += m0;
+        const hipError_t e = launch_gemm(bf, (const bf16*)A + m0 * lda, lda, Bt, bias,
+                                         R ? (const void*)((const bf16*)R + m0 * ldr) : nullptr, ldr,
+                                         (bf16*)C + m0 * ldc, ldc, mc, N, K, epi, s, lc);
+        if (e != hipSuccess) return e;
+      }
+      return hipSuccess;
+    }
+  }
   const bool aligned = (lda % 8 == 0) && (ldc % 8 == 0) && (ldr % 8 == 0) && (((uintptr_t)A & 15) == 0) &&
                        (((uintptr_t)Bt & 15) == 0) && (((uintptr_t)C & 15) == 0) && (((uintptr_t)R & 15) == 0) &&
-                       (((uintptr_t)bias & 15) == 0);
+                       (((uintptr_t)bias & 15) == 0) && (((uintptr_t)ln.g & 15) == 0) &&
+                       (((uintptr_t)ln.b & 15) == 0);
   if (N % GN != 0 || K % GK != 0 || !aligned)
-    return plain<bf16>(A, lda, Bt, bias, R, ldr, C, ldc, M, N, K, epi, s);
+    return plain<bf16>(A, lda, Bt, bias, R, ldr, C, ldc, M, N, K, epi, ln, s);
+  const bf16* a = (const bf16*)A;
+  const bf16* b = (const bf16*)Bt;
   // Persistent kernel: K a multiple of 128 and at least 256 (its load stream
   // runs three k steps ahead), element offsets within int32.
   if (N % PT == 0 && K % (2 * PK) == 0 && K >= 4 * PK && M >= 2048 && (long long)M * lda < (1ll << 31) &&
-      (long long)N * K < (1ll << 31)) {
+      (long long)M * ldc < (1ll << 31) && (long long)M * ldr < (1ll << 31) && (long long)N * K < (1ll << 31)) {
     // the current device's CU count, looked up once per device
     static std::atomic<int> cu_of_device[64];
     int dev = 0, n_cu = 0;
@@ -666,56 +654,29 @@ hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const fl
     const int tiles_n = N / PT, tiles_m = (M + PT - 1) / PT, n_tiles = tiles_n * tiles_m;
     const int per_xcd = (n_tiles + 7) / 8;
     const int grid = 8 * std::max(1, std::min(n_cu / 8, per_xcd));
-    const bf16* a = (const bf16*)A;
-    const bf16* b = (const bf16*)Bt;
-    const bf16* r = (const bf16*)R;
-    bf16* c = (bf16*)C;
-#define TX_GP4(E)                                                                                             \
-  gemm_bf16_p4<E><<<grid, 256, 0, s>>>(a, lda, b, bias, r, ldr, c, ldc, M, N, K, tiles_m, tiles_n, n_tiles, \
-                                       per_xcd)
+#define TX_GP4(E)                                                                                               \
+  gemm_bf16_p4<E><<<grid, 256, 0, s>>>(a, lda, b, bias, R, ldr, C, ldc, M, N, K, tiles_m, tiles_n, n_tiles, \
+                                       per_xcd, ln)
     switch (epi) {
       case EPI_BIAS: TX_GP4(EPI_BIAS); break;
       case EPI_BIAS_GELU: TX_GP4(EPI_BIAS_GELU); break;
       case EPI_BIAS_RESID: TX_GP4(EPI_BIAS_RESID); break;
+      case EPI_BIAS_RESLN: TX_GP4(EPI_BIAS_RESLN); break;
     }
 #undef TX_GP4
     return hipGetLastError();
   }
-  if (N % BN == 0 && M >= 2048) {
-    const int tiles_n = N / BN, tiles_m = (M + BM - 1) / BM, n_tiles = tiles_n * tiles_m;
-    const int grid = ((n_tiles + 7) / 8) * 8;
-    const bf16* a = (const bf16*)A;
-    const bf16* b = (const bf16*)Bt;
-    const bf16* r = (const bf16*)R;
-    bf16* c = (bf16*)C;
-#define TX_G256(E) \
-  gemm_bf16_mfma_256<E><<<grid, 512, 0, s>>>(a, lda, b, bias, r, ldr, c, ldc, M, N, K, tiles_m, tiles_n, n_tiles)
-    switch (epi) {
-      case EPI_BIAS: TX_G256(EPI_BIAS); break;
-      case EPI_BIAS_GELU: TX_G256(EPI_BIAS_GELU); break;
-      case EPI_BIAS_RESID: TX_G256(EPI_BIAS_RESID); break;
-    }
-#undef TX_G256
-    return hipGetLastError();
-  }
   const int tiles_n = N / GN, tiles_m = (M + GM - 1) / GM, n_tiles = tiles_n * tiles_m;
   const int grid = ((n_tiles + 7) / 8) * 8;
-  const bf16* a = (const bf16*)A;
-  const bf16* b = (const bf16*)Bt;
-  const bf16* r = (const bf16*)R;
-  bf16* c = (bf16*)C;
+#define TX_G128(E) \
+  gemm_bf16_mfma<E><<<grid, 256, 0, s>>>(a, lda, b, bias, R, ldr, C, ldc, M, N, K, tiles_n, n_tiles, ln)
   switch (epi) {
-    case EPI_BIAS:
-      gemm_bf16_mfma<EPI_BIAS><<<grid, 256, 0, s>>>(a, lda, b, bias, r, ldr, c, ldc, M, N, K, tiles_n, n_tiles);
-      break;
-    case EPI_BIAS_GELU:
-      gemm_bf16_mfma<EPI_BIAS_GELU><<<grid, 256, 0, s>>>(a, lda, b, bias, r, ldr, c, ldc, M, N, K, tiles_n, n_tiles);
-      break;
-    case EPI_BIAS_RESID:
-      gemm_bf16_mfma<EPI_BIAS_RESID><<<grid, 256, 0, s>>>(a, lda, b, bias, r, ldr, c, ldc, M, N, K, tiles_n,
-                                                          n_tiles);
-      break;
+    case EPI_BIAS: TX_G128(EPI_BIAS); break;
+    case EPI_BIAS_GELU: TX_G128(EPI_BIAS_GELU); break;
+    case EPI_BIAS_RESID: TX_G128(EPI_BIAS_RESID); break;
+    case EPI_BIAS_RESLN: TX_G128(EPI_BIAS_RESLN); break;
   }
+#undef TX_G128
   return hipGetLastError();
 }
 

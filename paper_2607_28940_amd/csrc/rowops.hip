@@ -1,5 +1,6 @@
 // Row-wise and data-movement kernels of the TransX path:
-//   LayerNorm of post-LN sublayers (Sec. 4.1.2 crossAttend block), optionally
+//   LayerNorm of post-LN sublayers (Sec. 4.1.2 crossAttend block) over the
+//   stored pre-LN sums, with its row statistics kept for later residuals, optionally
 //   fused with the decoder head (Sec. 4.1.3, Eq. action-decoding: either the
 //   softmax over k action embeddings, or with two actions one logit), the
 //   scatter of projected K/V rows into
@@ -51,12 +52,16 @@ __device__ __forceinline__ void head_out(const float (&z)[CNT], int c0, int stri
 // (EPL = d / 64). Each wave walks rows wave_id, wave_id + n_waves, ... so the
 // gain and bias it needs are loaded once, and the next row's features are
 // requested before the current row is normalised. Two-pass mean / variance
-// in fp32 from the register copy.
-template <typename T, int EPL, bool SCORE>
-__global__ __launch_bounds__(256) void layernorm_rows(const T* __restrict__ x, T* __restrict__ y,
-                                                      const float* __restrict__ g, const float* __restrict__ b,
-                                                      const float* __restrict__ w, const float* __restrict__ b0,
-                                                      float* __restrict__ scores, int M, int d, float eps, int n_act) {
+// in fp32 from the register copy. The input is the sublayer's pre-LN sum (sum
+// type TX); the output row goes out in the model type T, and the row's
+// statistics to `stats` (when given) for the epilogue that adds this LayerNorm
+// output as a residual later.
+template <typename TX, typename T, int EPL, bool SCORE>
+__global__ __launch_bounds__(256) void layernorm_rows(const TX* __restrict__ x, T* __restrict__ y,
+                                                      LnRow* __restrict__ stats, const float* __restrict__ g,
+                                                      const float* __restrict__ b, const float* __restrict__ w,
+                                                      const float* __restrict__ b0, float* __restrict__ scores, int M,
+                                                      int d, float eps, int n_act) {
   const int lane = threadIdx.x & 63;
   const int n_waves = gridDim.x * 4;
   int row = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -68,7 +73,7 @@ __global__ __launch_bounds__(256) void layernorm_rows(const T* __restrict__ x, T
     gv[e] = g[c0 + e];
     bv[e] = b[c0 + e];
   }
-  T nx[EPL];
+  TX nx[EPL];
 #pragma unroll
   for (int e = 0; e < EPL; ++e) nx[e] = x[(size_t)row * d + c0 + e];
   for (; row < M; row += n_waves) {
@@ -93,29 +98,31 @@ __global__ __launch_bounds__(256) void layernorm_rows(const T* __restrict__ x, T
     }
     sq = wave_sum(sq);
     const float inv = rsqrtf(sq / d + eps);
+    const float sh = -mean * inv;
     if (SCORE) {
       float z[EPL];
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) z[e] = (v[e] - mean) * inv * gv[e] + bv[e];
+      for (int e = 0; e < EPL; ++e) z[e] = fmaf(fmaf(v[e], inv, sh), gv[e], bv[e]);
       head_out<EPL>(z, c0, 1, EPL, lane, d, w, b0, scores, row, n_act);
     } else {
       T* yr = y + (size_t)row * d + c0;
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) yr[e] = (T)((v[e] - mean) * inv * gv[e] + bv[e]);
+      for (int e = 0; e < EPL; ++e) yr[e] = (T)fmaf(fmaf(v[e], inv, sh), gv[e], bv[e]);
+      if (stats && lane == 0) stats[row] = LnRow{inv, sh};
     }
   }
 }
 
 // Generic width: one wave per row, strided features, three passes over the row.
-template <typename T, bool SCORE>
-__global__ __launch_bounds__(256) void layernorm_rows_any(const T* __restrict__ x, T* __restrict__ y,
-                                                          const float* __restrict__ g, const float* __restrict__ b,
-                                                          const float* __restrict__ w, const float* __restrict__ b0,
-                                                          float* __restrict__ scores, int M, int d, float eps,
-                                                          int n_act) {
+template <typename TX, typename T, bool SCORE>
+__global__ __launch_bounds__(256) void layernorm_rows_any(const TX* __restrict__ x, T* __restrict__ y,
+                                                          LnRow* __restrict__ stats, const float* __restrict__ g,
+                                                          const float* __restrict__ b, const float* __restrict__ w,
+                                                          const float* __restrict__ b0, float* __restrict__ scores,
+                                                          int M, int d, float eps, int n_act) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= M) return;
-  const T* xr = x + (size_t)row * d;
+  const TX* xr = x + (size_t)row * d;
   float sum = 0.f;
   for (int c = lane; c < d; c += 64) sum += (float)xr[c];
   sum = wave_sum(sum);
@@ -127,8 +134,10 @@ __global__ __launch_bounds__(256) void layernorm_rows_any(const T* __restrict__ 
   }
   sq = wave_sum(sq);
   const float inv = rsqrtf(sq / d + eps);
+  const float sh = -mean * inv;
   if (!SCORE) {
-    for (int c = lane; c < d; c += 64) y[(size_t)row * d + c] = (T)(((float)xr[c] - mean) * inv * g[c] + b[c]);
+    for (int c = lane; c < d; c += 64) y[(size_t)row * d + c] = (T)fmaf(fmaf((float)xr[c], inv, sh), g[c], b[c]);
+    if (stats && lane == 0) stats[row] = LnRow{inv, sh};
     return;
   }
   // widths without a register-resident variant are at most 64 * 64 here
@@ -138,21 +147,22 @@ __global__ __launch_bounds__(256) void layernorm_rows_any(const T* __restrict__ 
 #pragma unroll
   for (int e = 0; e < MAXC; ++e) {
     const int c = lane + 64 * e;
-    z[e] = (e < cnt) ? ((float)xr[c] - mean) * inv * g[c] + b[c] : 0.f;
+    z[e] = (e < cnt) ? fmaf(fmaf((float)xr[c], inv, sh), g[c], b[c]) : 0.f;
   }
   head_out<MAXC>(z, lane, 64, cnt, lane, d, w, b0, scores, row, n_act);
 }
 
-template <typename T, bool SCORE>
-static hipError_t ln_dispatch(const void* x, void* y, const float* g, const float* b, const float* w, const float* b0,
-                              float* scores, int M, int d, float eps, int n_act, hipStream_t s) {
+template <typename TX, typename T, bool SCORE>
+static hipError_t ln_dispatch(const void* x, void* y, LnRow* stats, const float* g, const float* b, const float* w,
+                              const float* b0, float* scores, int M, int d, float eps, int n_act, hipStream_t s) {
   if (M <= 0) return hipSuccess;
   const int blocks = (M + 3) / 4;
   // register-resident widths: at most 8 rows per wave (2048 blocks of 4 waves)
   const int rblocks = std::min(blocks, std::max(2048, (blocks + 7) / 8));
-  const T* xx = (const T*)x;
+  const TX* xx = (const TX*)x;
   T* yy = (T*)y;
-#define TX_LN(E) layernorm_rows<T, E, SCORE><<<rblocks, 256, 0, s>>>(xx, yy, g, b, w, b0, scores, M, d, eps, n_act)
+#define TX_LN(E) \
+  layernorm_rows<TX, T, E, SCORE><<<rblocks, 256, 0, s>>>(xx, yy, stats, g, b, w, b0, scores, M, d, eps, n_act)
   switch (d) {
     case 64: TX_LN(1); break;
     case 128: TX_LN(2); break;
@@ -162,23 +172,23 @@ static hipError_t ln_dispatch(const void* x, void* y, const float* g, const floa
     case 2048: TX_LN(32); break;
     default:
       if (SCORE && d > 64 * 64) return hipErrorInvalidValue;
-      layernorm_rows_any<T, SCORE><<<blocks, 256, 0, s>>>(xx, yy, g, b, w, b0, scores, M, d, eps, n_act);
+      layernorm_rows_any<TX, T, SCORE><<<blocks, 256, 0, s>>>(xx, yy, stats, g, b, w, b0, scores, M, d, eps, n_act);
   }
 #undef TX_LN
   return hipGetLastError();
 }
 
-hipError_t launch_layernorm(bool bf, const void* x, void* y, const float* g, const float* b, int M, int d, float eps,
-                            hipStream_t s) {
-  return bf ? ln_dispatch<bf16, false>(x, y, g, b, nullptr, nullptr, nullptr, M, d, eps, 0, s)
-            : ln_dispatch<float, false>(x, y, g, b, nullptr, nullptr, nullptr, M, d, eps, 0, s);
+hipError_t launch_layernorm(bool bf, const void* x, void* y, LnRow* stats, const float* g, const float* b, int M,
+                            int d, float eps, hipStream_t s) {
+  return bf ? ln_dispatch<f16, bf16, false>(x, y, stats, g, b, nullptr, nullptr, nullptr, M, d, eps, 0, s)
+            : ln_dispatch<float, float, false>(x, y, stats, g, b, nullptr, nullptr, nullptr, M, d, eps, 0, s);
 }
 
 hipError_t launch_layernorm_score(bool bf, const void* x, const float* g, const float* b, const float* w,
                                   const float* b0, float* scores, int M, int d, float eps, int n_act, hipStream_t s) {
   if (n_act < 0 || n_act == 1 || n_act > 64) return hipErrorInvalidValue;
-  return bf ? ln_dispatch<bf16, true>(x, nullptr, g, b, w, b0, scores, M, d, eps, n_act, s)
-            : ln_dispatch<float, true>(x, nullptr, g, b, w, b0, scores, M, d, eps, n_act, s);
+  return bf ? ln_dispatch<f16, bf16, true>(x, nullptr, nullptr, g, b, w, b0, scores, M, d, eps, n_act, s)
+            : ln_dispatch<float, float, true>(x, nullptr, nullptr, g, b, w, b0, scores, M, d, eps, n_act, s);
 }
 
 // ---------------------------------------------------------------- cache scatter

@@ -12,6 +12,11 @@ typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+// Storage of a post-LN sublayer's pre-LayerNorm sum (bias + residual +
+// sublayer output) in bf16 models: 11 mantissa bits at the width of bf16.
+typedef _Float16 f16;
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int kPage = 64;  // tokens per cache page
@@ -91,17 +96,39 @@ struct PageGeom {
 // Every launcher returns hipSuccess or the launch error. Element type of the
 // activations is given by `bf16` (true) or fp32 (false).
 
-enum Epilogue { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2 };
+// Epilogues of C = A * Bt^T + bias:
+//   EPI_BIAS        C = acc + bias                          (C in the model type)
+//   EPI_BIAS_GELU   C = GELU(acc + bias)                    (C in the model type)
+//   EPI_BIAS_RESID  C = acc + bias + R, R in the model type (C in the sum type)
+//   EPI_BIAS_RESLN  C = acc + bias + LN(R), R in the sum type, where
+//                   LN(R)[m][n] = (R[m][n] * st[m].x + st[m].y) * g[n] + b[n]
+//                   recomputes in fp32 the LayerNorm output whose rounded copy
+//                   the sublayer read as its operand       (C in the sum type)
+// The sum type holds a post-LN sublayer's pre-LayerNorm sum: fp16 for bf16
+// models (same width, 8x finer rounding), fp32 for fp32 models.
+enum Epilogue { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2, EPI_BIAS_RESLN = 3 };
 
-// C[M][N] (ldc) = epi(A[M][K] (lda) * Bt[N][K]^T + bias[N] (+ R[M][N] (ldr))).
-// C must not overlap A or R (rows of a partial last tile rewrite row M - 1).
+// Row statistics of a LayerNorm in the form its consumers apply it:
+// x = 1 / sqrt(var + eps), y = -mean * x (so LN(v) = (v * x + y) * g + b).
+struct LnRow {
+  float x, y;
+};
+struct LnResid {
+  const LnRow* stats = nullptr;
+  const float* g = nullptr;
+  const float* b = nullptr;
+};
+
+// C[M][N] (ldc) = epi(A[M][K] (lda) * Bt[N][K]^T + bias[N] (+ residual)).
+// C must not overlap A or R.
 hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const float* bias, const void* R, int ldr,
-                       void* C, int ldc, int M, int N, int K, Epilogue epi, hipStream_t s);
+                       void* C, int ldc, int M, int N, int K, Epilogue epi, hipStream_t s, LnResid ln = LnResid());
 
-// y[i] = LN(x[i]) * g + b over d features, rows row0 .. row0+M-1
-hipError_t launch_layernorm(bool bf, const void* x, void* y, const float* g, const float* b, int M, int d,
-                            float eps, hipStream_t s);
-// Decoder head on LN(x[i]) = z_i (fp32 out): n_act == 0: scores[i] = z_i . w + b0;
+// y[i] = LN(x[i]) * g + b over d features for M rows; x in the sum type, y in
+// the model type; the row statistics go to stats[i] when it is not null.
+hipError_t launch_layernorm(bool bf, const void* x, void* y, LnRow* stats, const float* g, const float* b, int M,
+                            int d, float eps, hipStream_t s);
+// Decoder head on LN(x[i]) = z_i, x in the sum type (fp32 out): n_act == 0: scores[i] = z_i . w + b0;
 // n_act = k >= 2: scores[i][a] = softmax_a(z_i . w[a] + b0[a]), w fp32 [k][d].
 hipError_t launch_layernorm_score(bool bf, const void* x, const float* g, const float* b, const float* w,
                                   const float* b0, float* scores, int M, int d, float eps, int n_act, hipStream_t s);

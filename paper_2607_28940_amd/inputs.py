@@ -147,6 +147,9 @@ def make_weights(m: ModelConfig, variant: Sequence[str] = (), seed_w: int = SEED
     variant "sharp": attention Wq and Wk ~ N(0, (2/sqrt(d))^2) and the
       relative-position table ~ N(0, 1), so attention logits have std of a few
       units and softmax is far from uniform.
+    variant "sharp-cross": only the decoder cross-attention's Wq and Wk ~
+      N(0, (2/sqrt(d))^2): cross-attention logits of a few units over the
+      cached tokens, every other tensor at its base draw.
     variant "affine": LayerNorm gain 1 + N(0, 0.1), offset N(0, 0.1).
     The pooling vector of the global token is N(0, 0.02) (nearly uniform
     pooling), N(0, 16) under "sharp" (pooling logits of a few units); the
@@ -171,6 +174,8 @@ def make_weights(m: ModelConfig, variant: Sequence[str] = (), seed_w: int = SEED
         elif name == "W_dec" and ("sharp" in variant or "sharp-head" in variant):
             w = (4.0 / math.sqrt(d)) * z
         elif "sharp" in variant and name in ("Wq", "Wk", "sWq", "sWk", "xWq", "xWk"):
+            w = (2.0 / math.sqrt(d)) * z
+        elif "sharp-cross" in variant and name in ("xWq", "xWk"):
             w = (2.0 / math.sqrt(d)) * z
         else:
             w = 0.02 * z

@@ -10,23 +10,14 @@ import numpy as np
 from paper_2607_28940_amd import inputs as I
 
 FP32_TOL = 1e-4  # relative error bar for the fp32 model: every score
-BF16_TOL = 2e-2  # relative error bar for bf16 scores: the 99th percentile
-BF16_MAX = 3e-2  # cap on the largest bf16 score error
+BF16_TOL = 2e-2  # relative error bar for bf16 scores: every score
 
 
 def check_err(err: Dict[str, float], tol: float):
-    """Apply the bar of one comparison. fp32 (tol < BF16_TOL): every score
-    within tol. bf16: the 99th percentile within tol and the maximum within
-    BF16_MAX. The bf16 per-score error is the sum of some thirty independent
-    roundings to bf16 along the path (sigma ~ 5.5-6e-3 relative, p99
-    1.3-1.5e-2 measured), so the largest of N errors grows like
-    sqrt(2 ln N) sigma: ~3.5 sigma ~ 2e-2 at N ~ 1,000 compared scores, 3.9
-    sigma at 2,000. A bar on the maximum would be a bar on N; the stated 2e-2
-    therefore bounds the typical (p99) score and 3e-2 the extreme one."""
-    if tol < BF16_TOL:
-        assert err["max"] <= tol, err
-    else:
-        assert err["p99"] <= tol and err["max"] <= BF16_MAX, err
+    """Every compared score within tol (the error of each score is
+    |g - o| / max(|o|, rms(o)), see score_err). The 99th percentile is logged
+    beside the maximum."""
+    assert err["max"] <= tol, err
 
 
 def log(msg: str):
@@ -97,6 +88,17 @@ class DeviceCase:
         self.torch.cuda.synchronize()
         s = out.cpu().numpy().astype(np.float64)
         return [s[co[i]:co[i + 1]] for i in range(len(reqs))]
+
+
+def oracle_background(orc, wl: I.Workload, reqs: Sequence[int], append: bool = False):
+    """Start the oracle on the given requests in a worker thread (the oracle's
+    C code runs outside the GIL) while the GPU side proceeds; returns a future
+    of the list of their score arrays."""
+    from concurrent.futures import ThreadPoolExecutor
+    ex = ThreadPoolExecutor(1)
+    fut = ex.submit(lambda: [oracle_request(orc, wl, r, append=append)[0] for r in reqs])
+    ex.shutdown(wait=False)
+    return fut
 
 
 def oracle_request(orc, wl: I.Workload, r: int, append: bool = False, L: Optional[int] = None, cand=None):

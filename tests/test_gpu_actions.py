@@ -16,13 +16,8 @@ indexing and softmax at 1e-4). The bf16 cases keep the configurations'
 weights for the decoder body and sharpen only the action embeddings
 ("sharp-head"), so the probabilities stay far from uniform.
 
-The bf16 bar (2e-2) is stated for one scalar score per candidate. Every
-logit carries the same bf16 error as a scalar score (the candidate
-representation's rounding projected on one embedding: p99 1.3-1.5e-2 here, as
-for the scalar scores), so the logits take the scalar scores' rule
-(tests.parity_util.check_err): p99 <= 2e-2 and a maximum <= 3e-2, the
-extreme-value allowance for the ~2,000 logits of a case (measured maxima:
-1.7e-2 at k = 3, 2.4e-2 at k = 16)."""
+Every centred logit is held to the bar of a scalar score: within 2e-2
+(tests.parity_util.check_err)."""
 import dataclasses
 
 import numpy as np

@@ -83,9 +83,7 @@ def test_persistent_gemm_ragged_rows(O):
     wl = I.custom_workload(model, cfg_id=61, **GEMM_ROWS)
     rows, enc_rows = sum(wl.S) + sum(wl.C), sum(wl.L)
     assert rows >= 2048 and rows % 256 and enc_rows >= 2048 and enc_rows % 256
-    # standard weights: with the sharp variant bf16 rounding alone takes the
-    # largest sampled error to 2.05e-2, just over the 2e-2 bar
-    w = I.make_weights(model, ("affine",))
+    w = I.make_weights(model, ("sharp", "affine"))
     log(f"persistent GEMM rows: decoder {rows}, encoder {enc_rows}")
     big = DeviceCase(wl, w)
     big.build(range(wl.B))
@@ -117,7 +115,7 @@ def test_cache_contents_vs_oracle(O):
                 g = run.cache.export(r, part, layer).float().cpu().numpy()
                 e = tensor_err(g, ref[layer])
                 log(f"cache r{r} part{part} layer{layer}: {e:.3e}")
-                assert e < 5e-2, (r, part, layer, e)
+                assert e < 2e-2, (r, part, layer, e)
 
 
 @pytest.mark.parametrize("name,model", SMALL_BF16, ids=[m[0] for m in SMALL_BF16])

@@ -55,20 +55,16 @@ def test_tiny_fp32_sparse(oracle_mod):
 # a window ending on a page boundary (64, 128) and one straddling two pages (70)
 RAGGED = dict(L=[70, 1, 128, 10, 6, 64, 200], S=[5, 3, 0, 70, 2, 4, 9], C=[7, 1, 40, 33, 5, 64, 100])
 SHARP = ("sharp", "affine")
-# The window and page indexing is pinned at the fp32 bar with sharp attention
-# (logits of a few units: a misplaced key moves the scores far beyond 1e-4).
-# In bf16 the same sharp logits make the rounding of Q and K alone move the
-# softmax weights by percents; with few keys per query there is little
-# averaging, and a 64-token window reaches 2.3e-2 on one request of this
-# workload (the dense path 1.6e-2), so the bf16 64-token case uses the
-# standard attention weights and keeps the 2e-2 bar.
+# The window and page indexing is pinned at the fp32 bar and at the bf16 bar
+# with sharp attention (logits of a few units: a misplaced key moves the
+# scores far beyond either bar).
 CASES = [
     ("f32-dh64-L64-pool", ModelConfig(128, 2, 256, 1, 2, rel_pos_buckets=16, dtype="f32"), 64, True, SHARP,
      FP32_TOL),
     ("f32-dh32-L10-pool", ModelConfig(64, 2, 256, 1, 2, rel_pos_buckets=8, dtype="f32"), 10, True, SHARP, FP32_TOL),
     ("dh128-L10-pool", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16), 10, True, SHARP, BF16_TOL),
     ("dh64-L10-pool", ModelConfig(256, 4, 512, 2, 2, rel_pos_buckets=16), 10, True, SHARP, BF16_TOL),
-    ("dh128-L64-pool", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16), 64, True, ("affine",), BF16_TOL),
+    ("dh128-L64-pool", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16), 64, True, SHARP, BF16_TOL),
     ("dh64-L5-nopool", ModelConfig(256, 4, 512, 2, 1, rel_pos_buckets=0), 5, False, SHARP, BF16_TOL),
 ]
 
@@ -85,6 +81,14 @@ def test_sparse_ragged(oracle_mod, name, model, l_local, pool, variant, tol):
 
 
 def test_global_token_export_vs_oracle(oracle_mod):
+    """The pooled token's cross K/V rows against the oracle's, as max |error|
+    over rms. Cache rows elsewhere are held to 2e-2 (their own bf16 rounding,
+    up to ~4 rms x 2^-9, plus the ~4e-3 rms error of the encoded rows they
+    project). The pooled token is a softmax-weighted mean of encoded rows
+    whose pooling logits h . w / sqrt(d) have a spread of ~4 under "sharp"
+    (w ~ N(0, 16)): a relative error e of the rows moves each logit by ~4 e
+    and the weights by as much, so the token carries ~4x the rows' error; with
+    one 256-wide row per tensor the bar is 4e-2."""
     m = _sparse(ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16))
     wl = I.custom_workload(m, cfg_id=42, L=[150, 3], S=[2, 2], C=[3, 3])
     w = I.make_weights(m, ("sharp", "affine"))
@@ -99,7 +103,7 @@ def test_global_token_export_vs_oracle(oracle_mod):
                 g = run.cache.export(r, part, layer).float().cpu().numpy()
                 e = tensor_err(g, ref[layer])
                 log(f"global token r{r} part{part} layer{layer}: {e:.3e}")
-                assert e < 5e-2, (r, part, layer, e)
+                assert e < 4e-2, (r, part, layer, e)
 
 
 def test_sparse_append_folds_pooling_state(oracle_mod):
