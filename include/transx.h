@@ -13,6 +13,9 @@
  *   score_candidates  decoder over serving + candidate tokens, linear head
  *   score_events      the same per serving event of a user, each against its
  *                     own prefix of the cache (seq-to-seq training forward)
+ *   score_candidates_static
+ *                     score_candidates without a workspace argument and
+ *                     without allocating, for callers that cannot allocate
  *
  * Conventions
  *   - All tensors the caller hands over are device pointers unless marked
@@ -24,8 +27,10 @@
  *     throughout). Scores are always fp32.
  *   - The library never allocates device memory: the caller provides the
  *     repacked-weight buffer, the page pool and a workspace for each call.
- *     Host-side bookkeeping (page tables, free list, pinned staging for small
- *     uploads) is owned by the library.
+ *     (The one exception is the fixed array that score_candidates_static uses
+ *     in place of a workspace, part of the library's code object.) Host-side
+ *     bookkeeping (page tables, free list, pinned staging for small uploads)
+ *     is owned by the library.
  *   - Calls are asynchronous on the given stream. Build, append and score of the
  *     same request must be ordered on one stream by the caller. A handle must
  *     not be used from two host threads at once.
@@ -145,8 +150,10 @@ size_t tx_kv_page_bytes(const tx_config* cfg);
 size_t tx_kv_pool_bytes(const tx_config* cfg, int64_t n_pages, int32_t max_requests, int64_t max_tokens);
 
 /* Create a cache over a caller-owned device pool (256-byte aligned). Request
- * ids are 0 .. max_requests-1. Errors: TX_E_INVALID, TX_E_NOMEM (pool too
- * small). */
+ * ids are 0 .. max_requests-1. Also reserves the pinned host staging that
+ * score_candidates_static uploads its metadata through (4 x 512 KiB; without a
+ * usable device the cache is still created and that call later reports
+ * TX_E_NOMEM). Errors: TX_E_INVALID, TX_E_NOMEM (pool too small). */
 int tx_kv_cache_create(const tx_model* model, void* dev_pool, size_t pool_bytes, int64_t n_pages,
                        int32_t max_requests, int64_t max_tokens, tx_kv_cache** out);
 void tx_kv_cache_destroy(tx_kv_cache* cache);
@@ -248,6 +255,26 @@ int score_events(const tx_kv_cache* cache, int32_t n_events, const int32_t* req_
                  const int64_t* prefix_len /* host */, const void* serving, const int64_t* serving_offsets /* host */,
                  const void* candidates, const int64_t* candidate_offsets /* host */, float* scores, void* ws,
                  size_t ws_bytes, hipStream_t stream);
+
+/* score_candidates_static -- score_candidates for callers that cannot
+ * allocate device memory or call allocating routines: code under HIP graph
+ * capture, serving loops and harnesses that forbid allocation. Arguments,
+ * outputs and errors as in score_candidates, without the workspace: the call
+ * uses a fixed array of TX_STATIC_SCRATCH_BYTES (128 MiB) in the library's own
+ * device memory, one per GPU the library runs on, held from the library's
+ * first use on that GPU until the process ends, and the pinned staging for
+ * its metadata that tx_kv_cache_create reserved. A batch larger than the
+ * array runs in several passes over groups of requests; a request whose own
+ * activations or metadata exceed it is rejected with TX_E_NOMEM before any
+ * launch. It calls no hipMalloc, hipFree or other allocating routine. Every
+ * call on one GPU shares that GPU's array, which keeps the last call's
+ * contents (nothing in it needs to start at zero): calls that overlap on one
+ * GPU, on different streams or from different threads, race. The stream must
+ * belong to the current device (TX_E_INVALID otherwise). */
+#define TX_STATIC_SCRATCH_BYTES ((size_t)128 << 20)
+int score_candidates_static(const tx_kv_cache* cache, int32_t n_req, const int32_t* req_ids /* host */,
+                            const void* serving, const int64_t* serving_offsets /* host */, const void* candidates,
+                            const int64_t* candidate_offsets /* host */, float* scores, hipStream_t stream);
 
 /* ------------------------------------------------------------ measurement */
 

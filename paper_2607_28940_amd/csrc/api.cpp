@@ -47,6 +47,11 @@ int fail(int code, const char* fmt, ...) {
 
 size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
 
+// Pinned staging per ring slot reserved when a cache is created: the largest
+// per-pass metadata score_candidates_static uploads (its passes are planned
+// to fit).
+constexpr size_t kStagingReserve = 512 << 10;
+
 // Lays sub-buffers out in one device region (256-byte aligned); with a null
 // base it only measures.
 struct Carver {
@@ -312,8 +317,20 @@ struct Stager {
       if (s.host) (void)hipHostFree(s.host);
     }
   }
-  hipError_t acquire(size_t n, Slot** out) {
+  // Gives every slot an event and at least `cap` bytes of pinned memory.
+  hipError_t reserve(size_t cap) {
+    for (int i = 0; i < 4; ++i) {
+      Slot* s = nullptr;
+      hipError_t e = acquire(cap, &s, true);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
+  // The next slot of the ring, grown to n bytes if may_grow (a slot too small
+  // otherwise is hipErrorOutOfMemory: nothing is allocated).
+  hipError_t acquire(size_t n, Slot** out, bool may_grow) {
     Slot& s = slot[next];
+    if (!may_grow && (s.cap < n || !s.ev)) return hipErrorOutOfMemory;
     next = (next + 1) & 3;
     if (s.pending) {
       hipError_t e = hipEventSynchronize(s.ev);
@@ -336,10 +353,10 @@ struct Stager {
     *out = &s;
     return hipSuccess;
   }
-  hipError_t upload(void* dst, const void* src, size_t n, hipStream_t st) {
+  hipError_t upload(void* dst, const void* src, size_t n, hipStream_t st, bool may_grow = true) {
     if (n == 0) return hipSuccess;
     Slot* s = nullptr;
-    hipError_t e = acquire(n, &s);
+    hipError_t e = acquire(n, &s, may_grow);
     if (e != hipSuccess) return e;
     memcpy(s->host, src, n);
     e = hipMemcpyAsync(dst, s->host, n, hipMemcpyHostToDevice, st);
@@ -374,6 +391,7 @@ struct tx_kv_cache {
   std::vector<int64_t> len;  // -1: no cache
   std::vector<int32_t> free_list;
   mutable Stager st;  // metadata uploads also happen in const (score) calls
+  bool staging_reserved = false;  // the ring holds kStagingReserve bytes per slot
 };
 
 extern "C" {
@@ -437,6 +455,10 @@ int tx_kv_cache_create(const tx_model* m, void* dev_pool, size_t pool_bytes, int
   c->len.assign(max_requests, -1);
   c->free_list.resize(n_pages);
   for (int64_t i = 0; i < n_pages; ++i) c->free_list[i] = (int32_t)(n_pages - 1 - i);  // pop_back gives page 0 first
+  // pinned staging for the metadata of score_candidates_static, which may not
+  // allocate; without a usable device that call reports TX_E_NOMEM instead
+  c->staging_reserved = c->st.reserve(kStagingReserve) == hipSuccess;
+  if (!c->staging_reserved) (void)hipGetLastError();
   *out = c;
   return TX_OK;
 }
@@ -740,8 +762,10 @@ int64_t req_rows(int op, int i, const int64_t* a, const int64_t* b) {
 }
 
 // Split requests into consecutive groups that fit the workspace.
+// meta_cap bounds each pass's metadata (the uploads of the no-allocation
+// entry point go through fixed pinned staging).
 int plan_passes(const tx_model* m, int op, int n, const int64_t* a, const int64_t* b, size_t ws_bytes,
-                std::vector<int>& cuts) {
+                std::vector<int>& cuts, size_t meta_cap = SIZE_MAX) {
   cuts.assign(1, 0);
   int start = 0;
   int64_t rows = 0, mx = 0;
@@ -750,7 +774,10 @@ int plan_passes(const tx_model* m, int op, int n, const int64_t* a, const int64_
     if (pass_bytes(m, op, 1, r, r) > ws_bytes)
       return fail(TX_E_NOMEM, "workspace %zu bytes cannot hold request %d (%zu needed)", ws_bytes, i,
                   pass_bytes(m, op, 1, r, r));
-    if (i > start && pass_bytes(m, op, i - start + 1, rows + r, std::max(mx, r)) > ws_bytes) {
+    if (meta_bound(1, r, r, m->H) > meta_cap)
+      return fail(TX_E_NOMEM, "request %d: pass metadata above the %zu bytes of fixed staging", i, meta_cap);
+    if (i > start && (pass_bytes(m, op, i - start + 1, rows + r, std::max(mx, r)) > ws_bytes ||
+                      meta_bound(i - start + 1, rows + r, std::max(mx, r), m->H) > meta_cap)) {
       cuts.push_back(i);
       start = i;
       rows = 0;
@@ -1055,7 +1082,8 @@ namespace {
 // serving and candidate rows, decoded against the first kvlen[r] cached
 // tokens of request ids[r]).
 int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvlen, int a, int b, const char* xs,
-                   const int64_t* so, const char* xc, const int64_t* co, float* scores, char* ws, hipStream_t st) {
+                   const int64_t* so, const char* xc, const int64_t* co, float* scores, char* ws, hipStream_t st,
+                   bool fixed_staging) {
   const tx_model* m = c->m;
   const bool bf = m->bf;
   const int d = m->d, F = m->F, H = m->H;
@@ -1093,7 +1121,7 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
   const size_t o_tf = meta.put(t_full), o_tc = meta.put(t_cand), o_sf = meta.put(s_full), o_sc = meta.put(s_cand);
   const size_t mb = meta_bound(n, M64, mx, H);
   if (meta.buf.size() > mb) return fail(TX_E_NOMEM, "internal: metadata %zu > bound %zu", meta.buf.size(), mb);
-  TX_HIP(c->st.upload(ws, meta.buf.data(), meta.buf.size(), st));
+  TX_HIP(c->st.upload(ws, meta.buf.data(), meta.buf.size(), st, !fixed_staging));
   Carver cv(ws + mb);
   char* T = cv.take<char*>(M64 * d * es);
   char* QKV = cv.take<char*>(M64 * 3 * d * es);
@@ -1224,7 +1252,7 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
 // checked: offsets, pointers, workspace, then the passes.
 int score_groups(const tx_kv_cache* c, int n, const int32_t* ids, const int64_t* kvlen, const void* serving,
                  const int64_t* so, const void* cand, const int64_t* co, float* scores, void* ws, size_t ws_bytes,
-                 hipStream_t st) {
+                 hipStream_t st, bool fixed_staging = false) {
   TX_CHECK(check_offsets(so, n, "serving", 0));
   TX_CHECK(check_offsets(co, n, "candidate", 0));
   TX_CHECK(check_tokens(c, n, serving, so, "serving"));
@@ -1232,12 +1260,12 @@ int score_groups(const tx_kv_cache* c, int n, const int32_t* ids, const int64_t*
   if (co[n] > co[0] && !scores) return fail(TX_E_INVALID, "scores pointer is null");
   if (((uintptr_t)scores & 3)) return fail(TX_E_INVALID, "scores pointer misaligned");
   std::vector<int> cuts;
-  TX_CHECK(plan_passes(c->m, TX_OP_SCORE, n, so, co, ws_bytes, cuts));
+  TX_CHECK(plan_passes(c->m, TX_OP_SCORE, n, so, co, ws_bytes, cuts, fixed_staging ? kStagingReserve : SIZE_MAX));
   if (!ws) return fail(TX_E_INVALID, "workspace is null");
   TX_CHECK(check_weights(c));
   for (size_t p = 0; p + 1 < cuts.size(); ++p)
     TX_CHECK(run_score_pass(c, ids, kvlen, cuts[p], cuts[p + 1], (const char*)serving, so, (const char*)cand, co,
-                            scores, (char*)ws, st));
+                            scores, (char*)ws, st, fixed_staging));
   return TX_OK;
 }
 
@@ -1276,6 +1304,29 @@ int score_events(const tx_kv_cache* c, int32_t n, const int32_t* ids, const int6
                   i);
   }
   return score_groups(c, n, ids, prefix, serving, so, cand, co, scores, ws, ws_bytes, st);
+}
+
+int score_candidates_static(const tx_kv_cache* c, int32_t n, const int32_t* ids, const void* serving,
+                            const int64_t* so, const void* cand, const int64_t* co, float* scores, hipStream_t st) {
+  TX_CHECK(common_checks(c, n, ids, nullptr));
+  if (n == 0) return TX_OK;
+  std::vector<int64_t> kvlen(n);
+  for (int i = 0; i < n; ++i) {
+    if (c->len[ids[i]] < 1) return fail(TX_E_NOCACHE, "request %d has no cache", ids[i]);
+    kvlen[i] = c->len[ids[i]];
+  }
+  if (!c->staging_reserved)
+    return fail(TX_E_NOMEM, "no pinned staging was reserved when the cache was created (no usable device then)");
+  int dev = -1;
+  TX_HIP(hipGetDevice(&dev));
+  if (st) {
+    hipDevice_t sdev = -1;
+    TX_HIP(hipStreamGetDevice(st, &sdev));
+    if (sdev != dev) return fail(TX_E_INVALID, "stream belongs to device %d, the current device is %d", sdev, dev);
+  }
+  void* ws = nullptr;
+  TX_HIP(static_scratch(&ws));
+  return score_groups(c, n, ids, kvlen.data(), serving, so, cand, co, scores, ws, kStaticScratchBytes, st, true);
 }
 
 }  // extern "C"

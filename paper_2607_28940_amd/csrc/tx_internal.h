@@ -191,6 +191,12 @@ constexpr int kLgQueryBlock = 64;
 constexpr int kMaxActions = 16;  // largest supported action vocabulary of the decoder head
 constexpr int kMaxLocal = 64;  // largest supported l_local
 
+// Workspace of the no-allocation entry point: a fixed array in the library's
+// device memory, one per GPU, of kStaticScratchBytes. static_scratch() gives
+// the current device's address of it (looked up once per device).
+constexpr size_t kStaticScratchBytes = (size_t)128 << 20;
+hipError_t static_scratch(void** out);
+
 // dst[n][k] = src[k][n] (src [K][N] row-major), same element type
 hipError_t launch_transpose(bool bf, const void* src, void* dst, int K, int N, int dst_ld, hipStream_t s);
 // dst fp32 [N][K] = src [K][N]

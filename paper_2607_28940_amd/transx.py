@@ -77,6 +77,7 @@ _SIGS = {
     "kv_cache_build": (ctypes.c_int, [VP, ctypes.c_int32, I32P, VP, I64P, VP, ctypes.c_size_t, VP]),
     "kv_cache_append": (ctypes.c_int, [VP, ctypes.c_int32, I32P, VP, I64P, VP, ctypes.c_size_t, VP]),
     "score_candidates": (ctypes.c_int, [VP, ctypes.c_int32, I32P, VP, I64P, VP, I64P, VP, VP, ctypes.c_size_t, VP]),
+    "score_candidates_static": (ctypes.c_int, [VP, ctypes.c_int32, I32P, VP, I64P, VP, I64P, VP, VP]),
     "score_events": (ctypes.c_int, [VP, ctypes.c_int32, I32P, I64P, VP, I64P, VP, I64P, VP, VP, ctypes.c_size_t, VP]),
     "tx_profile_enable": (ctypes.c_int, [ctypes.c_int32]),
     "tx_profile_select": (ctypes.c_int, [ctypes.c_uint64]),
@@ -91,6 +92,7 @@ def header_functions() -> List[str]:
     """Names of the functions include/transx.h declares."""
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"^\s*#.*$", "", text, flags=re.M)  # preprocessor lines (macros)
     return sorted(set(re.findall(r"\b([A-Za-z_][A-Za-z0-9_]*)\s*\(", text)) -
                   {"if", "defined", "sizeof", "TRANSX_H"})
 
@@ -246,6 +248,20 @@ class KVCache:
         check(lib().score_candidates(self.handle, len(ids), _p(ids, I32P), VP(serving.data_ptr()), _p(so, I64P),
                                      VP(candidates.data_ptr()), _p(co, I64P), VP(out.data_ptr()), VP(ws.data_ptr()),
                                      n, VP(_stream(stream))))
+        return out
+
+    def score_static(self, req_ids, serving, serving_offsets, candidates, candidate_offsets, out=None, stream=None):
+        """score_candidates_static: no workspace argument, nothing allocated by
+        the library (its fixed device array serves as the workspace)."""
+        import torch
+        ids, so, co = _i32(req_ids), _i64(serving_offsets), _i64(candidate_offsets)
+        if out is None:
+            n = int(co[-1]) if len(co) else 0
+            k = self.model.mc.n_actions
+            out = torch.empty((n, k) if k else n, dtype=torch.float32, device=self.device)
+        check(lib().score_candidates_static(self.handle, len(ids), _p(ids, I32P), VP(serving.data_ptr()),
+                                            _p(so, I64P), VP(candidates.data_ptr()), _p(co, I64P),
+                                            VP(out.data_ptr()), VP(_stream(stream))))
         return out
 
     def score_events(self, req_ids, prefix_len, serving, serving_offsets, candidates, candidate_offsets, out=None,
