@@ -18,8 +18,9 @@ resident in HBM when it starts. Prints one JSON line.
 The JSON carries the roofline of the dominant kernel, whose per-launch time
 comes from HIP events the library records around its launches on the stream
 during the timed steps (tx_profile_*: a few untimed steps with every launch
-bracketed pick that kernel and give the per-class table first), and the fp64
-CPU oracle's own throughput on a bounded sample.
+bracketed pick that kernel and give the per-class table first), the minimum,
+median and maximum of the timed steps' own times, and the fp64 CPU oracle's
+own throughput on a bounded sample.
 """
 from __future__ import annotations
 
@@ -254,15 +255,18 @@ def main():
         dom = max(prof_all, key=lambda k: prof_all[k]["ms"])
         T.profile_enable(True)
         T.profile_select([dom])
+    # one event between consecutive steps: the whole timed region and every
+    # step's own time (its distribution goes into the JSON line)
     stream = torch.cuda.current_stream()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    ev0.record(stream)
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for k in range(args.steps):
         step()
-    ev1.record(stream)
+        evs[k + 1].record(stream)
     torch.cuda.synchronize()
-    ms = ev0.elapsed_time(ev1) / args.steps
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    step_ms = sorted(evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps))
     prof = {}
     if not args.no_profile:
         prof = T.profile_read()
@@ -342,7 +346,10 @@ def main():
     line = {
         "metric": metric,
         "value": round(value, 1), "unit": "scores/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "ms_per_step": round(ms, 4),
+        "step_ms": {"min": round(step_ms[0], 4), "median": round(float(np.median(step_ms)), 4),
+                    "max": round(step_ms[-1], 4)},
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": m.dtype, "data": "synthetic (seeded N(0,1) tokens, N(0,0.02) weights)",
         "config": {"workload": f"{args.workload}: B={wl.B} L={'ragged' if len(set(wl.L)) > 1 else wl.L[0]} "
                                f"S={'ragged' if len(set(wl.S)) > 1 else wl.S[0]} "

@@ -34,9 +34,14 @@
  *   - Calls are asynchronous on the given stream. Build, append and score of the
  *     same request must be ordered on one stream by the caller. A handle must
  *     not be used from two host threads at once.
- *   - Every argument check runs on the host before any launch; a call that
- *     returns an error has changed nothing. tx_last_error() describes the last
- *     error of the calling thread.
+ *   - Every argument check runs on the host before any launch: a call that
+ *     returns TX_E_INVALID, TX_E_NOMEM, TX_E_NOCACHE or TX_E_UNSUPPORTED has
+ *     changed nothing. When a HIP call fails inside kv_cache_build or
+ *     kv_cache_append (TX_E_HIP), the call's requests are left without a cache
+ *     (length -1) and keep their pages until tx_kv_cache_release returns them
+ *     to the free list (work already enqueued on the stream may still write
+ *     to them); the other requests are untouched. tx_last_error() describes
+ *     the last error of the calling thread.
  */
 #ifndef TRANSX_H
 #define TRANSX_H

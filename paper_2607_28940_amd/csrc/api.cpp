@@ -1028,10 +1028,13 @@ int kv_cache_build(tx_kv_cache* c, int32_t n, const int32_t* ids, const void* X,
       c->free_list.pop_back();
       c->h_table[(size_t)ids[i] * c->max_pages + k] = pg.back();
     }
-    c->len[ids[i]] = 0;
   }
-  TX_HIP(c->st.upload(c->d_table, c->h_table.data(), c->h_table.size() * 4, st));
-  const int rc = encode_call(c, TX_OP_BUILD, n, ids, X, off, ws, ws_bytes, st);
+  // from here on a failure leaves these requests without a cache, holding
+  // their pages until release
+  int rc = TX_OK;
+  const hipError_t e = c->st.upload(c->d_table, c->h_table.data(), c->h_table.size() * 4, st);
+  if (e != hipSuccess) rc = fail(TX_E_HIP, "page table upload failed: %s", hipGetErrorString(e));
+  if (rc == TX_OK) rc = encode_call(c, TX_OP_BUILD, n, ids, X, off, ws, ws_bytes, st);
   for (int i = 0; i < n; ++i) c->len[ids[i]] = rc == TX_OK ? off[i + 1] - off[i] : -1;
   return rc;
 }
@@ -1067,8 +1070,12 @@ int kv_cache_append(tx_kv_cache* c, int32_t n, const int32_t* ids, const void* X
       c->h_table[(size_t)ids[i] * c->max_pages + pg.size() - 1] = pg.back();
     }
   }
-  TX_HIP(c->st.upload(c->d_table, c->h_table.data(), c->h_table.size() * 4, st));
-  const int rc = encode_call(c, TX_OP_APPEND, n, ids, X, off, ws, ws_bytes, st);
+  // from here on a failure leaves these requests without a cache, holding
+  // their pages until release
+  int rc = TX_OK;
+  const hipError_t e = c->st.upload(c->d_table, c->h_table.data(), c->h_table.size() * 4, st);
+  if (e != hipSuccess) rc = fail(TX_E_HIP, "page table upload failed: %s", hipGetErrorString(e));
+  if (rc == TX_OK) rc = encode_call(c, TX_OP_APPEND, n, ids, X, off, ws, ws_bytes, st);
   for (int i = 0; i < n; ++i) c->len[ids[i]] = rc == TX_OK ? c->len[ids[i]] + off[i + 1] - off[i] : -1;
   return rc;
 }

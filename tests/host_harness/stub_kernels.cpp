@@ -1,0 +1,54 @@
+// Host-only stand-ins for the library's kernel launchers, linked with the
+// real api.cpp into a test library: every launcher returns success without
+// touching memory, so the host logic (checks, page bookkeeping, pass
+// planning, error paths) runs on a machine without a GPU, and the first HIP
+// runtime call that needs a device fails where a device fault would.
+// Test infrastructure only; never part of libtransx.so.
+#include "../../paper_2607_28940_amd/csrc/tx_internal.h"
+
+namespace tx {
+
+hipError_t launch_gemm(bool, const void*, int, const void*, const float*, const void*, int, void*, int, int, int, int,
+                       Epilogue, hipStream_t, LnResid) {
+  return hipSuccess;
+}
+hipError_t launch_layernorm(bool, const void*, void*, LnRow*, const float*, const float*, int, int, float,
+                            hipStream_t) {
+  return hipSuccess;
+}
+hipError_t launch_layernorm_score(bool, const void*, const float*, const float*, const float*, const float*, float*,
+                                  int, int, float, int, hipStream_t) {
+  return hipSuccess;
+}
+hipError_t launch_paged_attention(bool, const void*, int, void*, int, const void*, const int32_t*, int, PageGeom, int,
+                                  const AttnReq*, const AttnTile*, int, bool, const float*, int, int, hipStream_t) {
+  return hipSuccess;
+}
+int paged_attention_q_block(bool, int) { return 128; }
+hipError_t launch_self_attention(bool, const void*, int, int, void*, const SelfReq*, const SelfTile*, int, bool,
+                                 hipStream_t) {
+  return hipSuccess;
+}
+int self_attention_q_block(bool, int) { return 128; }
+hipError_t launch_scatter_kv(bool, const void*, int, int, int, void*, const int32_t*, int, PageGeom,
+                             const ScatterTile*, int, hipStream_t) {
+  return hipSuccess;
+}
+hipError_t launch_export_kv(bool, const void*, const int32_t*, PageGeom, int, int, int64_t, void*, hipStream_t) {
+  return hipSuccess;
+}
+hipError_t launch_pool(bool, const void*, int, const float*, float, const PoolChunk*, int, const PoolReq*, int, float*,
+                       float*, float*, void*, hipStream_t) {
+  return hipSuccess;
+}
+hipError_t launch_store_rows(bool, const void*, int, const PoolReq*, int, void*, hipStream_t) { return hipSuccess; }
+hipError_t launch_lg_attention(bool, const void*, int, void*, int, const void*, const int32_t*, int, PageGeom, int,
+                               const AttnReq*, const AttnTile*, int, int, const void*, int, int, hipStream_t) {
+  return hipSuccess;
+}
+hipError_t static_scratch(void**) { return hipErrorNoDevice; }
+hipError_t launch_transpose(bool, const void*, void*, int, int, int, hipStream_t) { return hipSuccess; }
+hipError_t launch_transpose_to_f32(bool, const void*, float*, int, int, hipStream_t) { return hipSuccess; }
+hipError_t launch_to_f32(bool, const void*, float*, int64_t, hipStream_t) { return hipSuccess; }
+
+}  // namespace tx
