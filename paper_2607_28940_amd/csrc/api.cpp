@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -16,6 +17,7 @@
 #pragma GCC visibility pop
 
 #include "tx_internal.h"
+#include "xplan.h"
 
 using namespace tx;
 
@@ -650,14 +652,38 @@ struct Meta {
   }
 };
 
+// kv-split of the pipelined cross-attention: partial slots per pass (each
+// kXPartBytes of workspace).
+constexpr int kXMaxParts = 512;
+
 // Generous upper bound of a pass's metadata bytes.
 size_t meta_bound(int n_req, int64_t rows, int64_t max_rows, int H) {
   const int64_t tiles = (int64_t)H * (rows / 32 + n_req + 1) + 8 * (max_rows / 32 + 2);
   const int64_t pool_chunks = rows / 64 + n_req + 1;
   const int64_t page_tiles = rows / kPage + n_req + 1;  // each request adds at most one partial page
+  // cross-attention tiles (whole and split sets together), per-XCD offsets
+  // and merges of both decoder layer kinds, with the alignment of their ten
+  // arrays
+  const int64_t xtiles = (int64_t)H * (rows / kXQueryBlock + n_req + 1) + kXMaxParts;  // per layer kind
   return align_up(8192 + (size_t)n_req * 160 + (size_t)tiles * sizeof(AttnTile) * 6 +
                   (size_t)pool_chunks * sizeof(PoolChunk) + (size_t)n_req * sizeof(PoolReq) +
-                  (size_t)page_tiles * sizeof(ScatterTile));
+                  (size_t)page_tiles * sizeof(ScatterTile) + 2 * (size_t)xtiles * sizeof(XTile) +
+                  2 * (size_t)kXMaxParts * sizeof(XMerge) + 4 * 9 * sizeof(int32_t) + 10 * 256);
+}
+
+// Resident blocks of the cross-attention on the current device (kXBlocksPerCu
+// per CU), the CU count looked up once per device.
+int xattn_resident_blocks() {
+  static std::atomic<int> cu_of_device[64];
+  int dev = 0, n_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = -1;
+  if (dev >= 0) n_cu = cu_of_device[dev].load(std::memory_order_relaxed);
+  if (n_cu <= 0) {
+    if (dev < 0 || hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 8)
+      n_cu = 256;
+    if (dev >= 0) cu_of_device[dev].store(n_cu, std::memory_order_relaxed);
+  }
+  return n_cu / 8 * 8 * kXBlocksPerCu;
 }
 
 // Attention worklist: tiles of q_block queries for every (request, head),
@@ -751,9 +777,16 @@ size_t pool_pass_bytes(const tx_model* m, int op, int n, int64_t rows) {
          align_up((size_t)n * 2 * m->n_dec * d * m->esz) + 3 * 256;
 }
 
+// The dense bf16 d_h = 128 decoder cross-attention runs on the tile list of
+// xattn_plan (with kv-split); its partial slots take a fixed workspace area.
+bool xattn_pipe_used(const tx_model* m) { return m->l_local == 0 && cross_attention_split_ok(m->bf, m->dh); }
+size_t xattn_part_area(const tx_model* m, int op) {
+  return op == TX_OP_SCORE && xattn_pipe_used(m) ? align_up((size_t)kXMaxParts * kXPartBytes) : 0;
+}
+
 size_t pass_bytes(const tx_model* m, int op, int n, int64_t rows, int64_t max_rows) {
-  return meta_bound(n, rows, max_rows, m->H) + align_up(rows * row_bytes(m, op)) + 10 * 256 +
-         pool_pass_bytes(m, op, n, rows);
+  return meta_bound(n, rows, max_rows, m->H) + align_up(rows * row_bytes(m, op)) + 11 * 256 +
+         pool_pass_bytes(m, op, n, rows) + xattn_part_area(m, op);
 }
 
 // rows of request i for the op
@@ -1117,15 +1150,30 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
   const int sqb = self_attention_q_block(bf, m->dh);
   std::vector<AttnTile> t_full, t_cand;
   std::vector<SelfTile> s_full, s_cand;
+  const bool xpipe = xattn_pipe_used(m);
+  const int xblocks = xpipe ? xattn_resident_blocks() : 0;
+  XPlan x_full, x_cand;
   if (m->n_dec > 1) {
-    attn_tiles(full, H, qb, false, t_full);
+    if (xpipe) xattn_plan(full, H, xblocks, kXMaxParts, x_full);
+    else attn_tiles(full, H, qb, false, t_full);
     self_tiles(sreq, H, sqb, false, s_full);
   }
-  attn_tiles(cand, H, qb, false, t_cand);
+  if (xpipe) xattn_plan(cand, H, xblocks, kXMaxParts, x_cand);
+  else attn_tiles(cand, H, qb, false, t_cand);
   self_tiles(sreq, H, sqb, true, s_cand);
   Meta meta;
   const size_t o_sreq = meta.put(sreq), o_full = meta.put(full), o_cand = meta.put(cand);
   const size_t o_tf = meta.put(t_full), o_tc = meta.put(t_cand), o_sf = meta.put(s_full), o_sc = meta.put(s_cand);
+  // cross-attention tile sets on the device: whole-request tiles, their
+  // per-XCD offsets, kv-split tiles, theirs, and the merge items
+  struct XDev {
+    size_t wt, wo, st, so, mg;
+  };
+  auto put_plan = [&](const XPlan& xp) {
+    return XDev{meta.put(xp.whole.tiles), meta.put(xp.whole.xoff), meta.put(xp.split.tiles), meta.put(xp.split.xoff),
+                meta.put(xp.merges)};
+  };
+  const XDev xd_full = put_plan(x_full), xd_cand = put_plan(x_cand);
   const size_t mb = meta_bound(n, M64, mx, H);
   if (meta.buf.size() > mb) return fail(TX_E_NOMEM, "internal: metadata %zu > bound %zu", meta.buf.size(), mb);
   TX_HIP(c->st.upload(ws, meta.buf.data(), meta.buf.size(), st, !fixed_staging));
@@ -1139,6 +1187,7 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
   char* Ys[2] = {cv.take<char*>(M64 * d * es), cv.take<char*>(M64 * d * es)};
   LnRow* Ss[2] = {cv.take<LnRow*>(M64 * sizeof(LnRow)), cv.take<LnRow*>(M64 * sizeof(LnRow))};
   char* Hf = cv.take<char*>(M64 * F * es);
+  float* xpart = xpipe ? cv.take<float*>(kXMaxParts * kXPartBytes) : nullptr;
   // The first layer reads the serving and candidate tokens where they are
   // (its QKV GEMM and the self-attention output GEMM's residual run once per
   // token array) when the bf16 GEMMs can take them (16-byte aligned rows) and
@@ -1175,6 +1224,8 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
   for (int l = 0; l < m->n_dec; ++l) {
     const DecLayer& L = m->dec[l];
     const bool last = l == m->n_dec - 1;
+    const XPlan& xp = last ? x_cand : x_full;
+    const XDev& xd = last ? xd_cand : xd_full;
     // rows from r0 on continue past the self-attention: all rows, or only the
     // candidates in the last layer (serving rows there only supply keys/values)
     const int r0 = last ? (int)Ms : 0, Mr = M - r0;
@@ -1229,6 +1280,11 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
               sparse ? launch_lg_attention(bf, A, d, O, d, c->pool, c->d_table, c->max_pages, c->geom, m->n_enc + l,
                                            areq, at, n_at, m->l_local, m->gpool ? c->d_gkv : nullptr,
                                            2 * m->n_dec * d, l, st)
+              : xpipe ? launch_cross_attention(
+                            A, d, O, d, c->pool, c->d_table, c->max_pages, c->geom, m->n_enc + l,
+                            (const XTile*)(ws + xd.wt), (const int32_t*)(ws + xd.wo), xp.whole.longest(),
+                            (const XTile*)(ws + xd.st), (const int32_t*)(ws + xd.so), xp.split.longest(), xpart,
+                            (const XMerge*)(ws + xd.mg), (int)xp.merges.size(), st)
                      : launch_paged_attention(bf, A, d, O, d, c->pool, c->d_table, c->max_pages, c->geom,
                                               m->n_enc + l, areq, at, n_at, false, nullptr, 0, qb, st));
     TX_LAUNCH(K_GEMM_XO, xo.first, xo.second,

@@ -83,7 +83,8 @@ __device__ __forceinline__ void pace_lds_reads() {
 // First half: S^T = K Q^T, the online softmax update and P^T in bf16.
 template <int DH, bool FROM_LDS, class KFrag, class Mask>
 __device__ __forceinline__ void mfma_qk_softmax(KFrag kfrag, const bf16x8 (&qf)[DH / 16], MfmaAcc<DH>& acc,
-                                                float scale_log2, int hi, bool masked, Mask mask, bf16x8 (&pf)[4]) {
+                                                float scale_log2, int hi, bool masked, Mask mask, bf16x8 (&pf)[4],
+                                                float thr = -1.f) {
   floatx16 s[2];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
@@ -109,7 +110,8 @@ __device__ __forceinline__ void mfma_qk_softmax(KFrag kfrag, const bf16x8 (&qf)[
   // reference m that only moves when this tile would push one above 2^8
   // (fine for fp32 sums and bf16 P); O and l are rescaled only then. The
   // final O / l does not depend on which reference was used.
-  const bool bump = mx > acc.m + 8.f / scale_log2;
+  // (thr, when given, is 8 / scale_log2 computed once by the caller)
+  const bool bump = mx > acc.m + (thr >= 0.f ? thr : 8.f / scale_log2);
   if (__any(bump)) {
     const float m_new = bump ? mx : acc.m;
     // 1 where the reference stays (also at -inf), 0 where it leaves -inf
@@ -376,7 +378,7 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
 }
 
 // ============================================================================
-// The same cross-attention (no causal mask, d_h = 128) with three blocks per
+// The decoder cross-attention (no causal mask, d_h = 128) with three blocks per
 // CU, i.e. three waves per SIMD to overlap each wave's dependent page chain
 // (QK on MFMA, softmax on the VALU, PV on MFMA) with two others instead of
 // one: 48 KB of LDS (K double-buffered, V^T single-buffered) and at most 168
@@ -384,29 +386,39 @@ __global__ __launch_bounds__(256, 2) void paged_attn_mfma(const bf16* __restrict
 // p + 1's V^T once page p's PV has left the buffer; before the PV each wave
 // waits for its own V^T loads only (the K loads issued after them may stay in
 // flight) and the block meets at a barrier. Same arithmetic in the same order
-// as paged_attn_mfma, so the outputs are bitwise identical.
+// as paged_attn_mfma.
+// The tiles come as one list per XCD (XCD x: tiles[xoff[x] .. xoff[x + 1])).
+// A tile (XTile) covers up to 128 queries of one request and head against the
+// key pages page_begin .. page_end - 1: all of the request's pages (its rows
+// are written normalised), or one part of them (a kv-split tile: the
+// unnormalised output, reference max and running sum go to a partial slot,
+// combined later by xattn_merge). Keys past the request's length on its last
+// page are masked; the cache keeps zeros in their V^T columns (the page
+// scatter writes them), so their zero probabilities never meet other values.
 // ============================================================================
-template <int DH>
+template <int DH, bool SPLIT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) void paged_attn_mfma3(
     const bf16* __restrict__ q, int ldq, bf16* __restrict__ out, int ldo, const bf16* __restrict__ pool,
     const int32_t* __restrict__ page_table, int max_pages, PageGeom g, int layer_slot,
-    const AttnReq* __restrict__ reqs, const AttnTile* __restrict__ tiles, float scale_log2) {
-  constexpr int KLD = DH, VLD = 64;
+    const XTile* __restrict__ tiles, const int32_t* __restrict__ xoff, float* __restrict__ partial,
+    float scale_log2, float bump_thr) {
   // K page buffers 0, 1, then the V^T page buffer
   __shared__ __attribute__((aligned(16))) bf16 sKV[3 * 64 * DH];
   bf16* const sK0 = sKV;
   bf16* const sK1 = sKV + 64 * DH;
   bf16* const sV = sKV + 2 * 64 * DH;
 
-  const AttnTile tile = tiles[blockIdx.x];
-  if (tile.q_count <= 0) return;
-  const AttnReq rq = reqs[tile.req];
+  // block b runs on XCD b % 8 and takes entry b / 8 of that XCD's tile list
+  const int t_idx = xoff[blockIdx.x & 7] + (int)(blockIdx.x >> 3);
+  if (t_idx >= xoff[(blockIdx.x & 7) + 1]) return;
+  const XTile tile = tiles[t_idx];
   const int h = tile.head;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform in its wave: a scalar, as is all derived from it
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hi = lane >> 5;
   const bool wave_active = wave * 32 < tile.q_count;
   const int i = tile.q_begin + min(wave * 32 + l32, tile.q_count - 1);
-  const int row = i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
+  const int row = i < tile.qa_n ? tile.qa_row + i : tile.qb_row + (i - tile.qa_n);
 
   bf16x8 qf[DH / 16];
   {
@@ -417,65 +429,163 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))) voi
   MfmaAcc<DH> acc;
   acc.init();
 
-  const int kv_len = rq.kv_len;
-  const int n_pages = (kv_len + kPage - 1) / kPage;
-  const bool partial = kv_len % kPage != 0;
-  const int32_t* ptab = page_table + (size_t)rq.slot * max_pages;
+  const int kv_len = tile.kv_len;
+  const int p0 = tile.page_begin, n_pages = tile.page_end - tile.page_begin;
+  const int32_t* ptab = page_table + (size_t)tile.slot * max_pages + p0;
   const PageDma<DH> pd(wave, lane);
-  auto page = [&](int p) { return pool + (size_t)ptab[p] * g.page_elems; };
-  auto zero_tail = [&](int p) {
-    const int valid = kv_len - p * kPage;
-    for (int e = tid; e < DH * 64; e += 256) {
-      const int r = e >> 6, col = e & 63;
-      const int chunk = (col >> 3) ^ ((r >> 1) & 7);
-      if (vt_col(chunk * 8 + (col & 7)) >= valid) sV[e] = (bf16)0.f;
-    }
-  };
+  // page-table window: lane l holds the pool index of page wbase + l of the
+  // range; a page's index is read from its lane into a scalar, so the page
+  // loads take a uniform address and no memory read of their own
+  int wbase = 0;
+  int pwin = ptab[min(lane, n_pages - 1)];
+  auto page = [&](int p) { return pool + (size_t)__builtin_amdgcn_readlane(pwin, p - wbase) * g.page_elems; };
   pd.load(page(0) + g.k_off(layer_slot, h), pd.koff, sK0);
   pd.load(page(0) + g.v_off(layer_slot, h), pd.voff, sV);
+  // LDS byte offsets of the lane's MFMA fragments, the swizzles of k_frag
+  // and v_frag in closed form: K row kb * 32 + l32, slot 2 kk + hi at
+  // kb * 64 DH * 2 + (kxor ^ 32 kk); V^T row 32 db + l32, slot 2 ks + hi at
+  // db * 4096 + (vxor ^ 32 ks). One register each; every read costs one XOR.
+  const int kxor = (l32 * DH * 2) | ((hi ^ (l32 & (DH / 8 - 1))) << 4);
+  const int vxor = (l32 * 128) | ((hi ^ ((l32 >> 1) & 7)) << 4);
+  const char* const lds = reinterpret_cast<const char*>(sKV);
   __syncthreads();
-  if (n_pages == 1 && partial) {
-    zero_tail(0);
-    __syncthreads();
-  }
   for (int p = 0; p < n_pages; ++p) {
     const int b = (p & 1) * (64 * DH);
-    const bf16* cK = sK0 + b;
     if (p + 1 < n_pages) pd.load(page(p + 1) + g.k_off(layer_slot, h), pd.koff, sK0 + (64 * DH - b));
-    const int key0 = p * kPage;
+    const int key0 = (p0 + p) * kPage;
     bf16x8 pf[4];
+    // the K buffer's offset joins the base before the XORs (it lies above
+    // their bits); the opaque copies keep the per-read addresses from being
+    // hoisted out of the loop into registers held across it
+    int kx = kxor + 2 * b, vx = vxor + 2 * 2 * 64 * DH;
+    asm volatile("" : "+v"(kx), "+v"(vx));
     if (wave_active) {
       auto kfrag = [&](int kb, int kk) {
-        return *reinterpret_cast<const bf16x8*>(&cK[k_frag<DH, KLD, true>(kb * 32 + l32, 2 * kk + hi)]);
+        return *reinterpret_cast<const bf16x8*>(lds + (kx ^ (32 * kk)) + kb * 64 * DH);
       };
       mfma_qk_softmax<DH, true>(kfrag, qf, acc, scale_log2, hi, key0 + kPage > kv_len, [&](int kl, float x) {
         return key0 + kl < kv_len ? x : -INFINITY;
-      }, pf);
+      }, pf, bump_thr);
     }
     if (p > 0) {
       // V^T of page p (requested after page p - 1's PV) in LDS for every wave;
       // the DH / 32 K loads of page p + 1 issued since may stay in flight
       if (p + 1 < n_pages) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(DH / 32) : "memory");
       else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
-      if (p + 1 == n_pages && partial) {
-        zero_tail(p);
-        __syncthreads();
-      }
     }
     if (wave_active) {
       auto vfrag = [&](int ks, int db) {
-        const int kbase = (ks >> 1) * 32 + 16 * (ks & 1) + 8 * hi;  // in the V^T tile's permuted key order
-        return *reinterpret_cast<const bf16x8*>(&sV[v_frag<VLD, true>(32 * db + l32, kbase >> 3)]);
+        return *reinterpret_cast<const bf16x8*>(lds + (vx ^ (32 * ks)) + db * 4096);
       };
       mfma_pv<DH, true>(vfrag, pf, acc);
     }
     __syncthreads();  // K and V^T of page p no longer read; K of page p + 1 landed
+    // no load is in flight here: the window moves when the next body's K
+    // load (page p + 2) would leave it
+    if (p + 2 - wbase >= 64 && p + 2 < n_pages) {
+      wbase = p + 1;
+      pwin = ptab[min(p + 1 + lane, n_pages - 1)];
+      // consumed here, where it is the only load in flight (so that no later
+      // read of the window waits on the page loads issued after it)
+      asm volatile("" : "+v"(pwin));
+    }
     if (p + 1 < n_pages) pd.load(page(p + 1) + g.v_off(layer_slot, h), pd.voff, sV);
+  }
+  if (SPLIT) {
+    // kv-split tile: fp32 O (unnormalised, features 32 db + 8 gq + 4 hi ..),
+    // reference max and running sum of each of the wave's queries
+    const int lq = wave * 32 + l32;
+    if (lq < tile.q_count) {
+      float* ps = partial + (size_t)tile.part * (128 * (DH + 2));
+#pragma unroll
+      for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq) {
+          const floatx4 w = {acc.o[db][4 * gq], acc.o[db][4 * gq + 1], acc.o[db][4 * gq + 2], acc.o[db][4 * gq + 3]};
+          *reinterpret_cast<floatx4*>(ps + (size_t)lq * DH + 32 * db + 8 * gq + 4 * hi) = w;
+        }
+      if (hi == 0) {
+        ps[128 * DH + lq] = acc.m;
+        ps[128 * DH + 128 + lq] = acc.l;
+      }
+    }
+    return;
   }
   // every body ends on a barrier and the last requests nothing: waves 0-1
   // park their output rows in K buffer 0, waves 2-3 in K buffer 1
   mfma_store_out_staged<DH>(acc, (wave < 2 ? sK0 : sK1) + (wave & 1) * 32 * DH, out, ldo, h * DH, lane,
-                            tile.q_begin + wave * 32, tile.q_count - wave * 32, rq.qa_n, rq.qa_row, rq.qb_row);
+                            tile.q_begin + wave * 32, tile.q_count - wave * 32, tile.qa_n, tile.qa_row, tile.qb_row);
+}
+
+// ============================================================================
+// Log-sum-exp merge of kv-split partial results: for every query of a
+// (request, head, query block) split over n_parts page ranges,
+//   O = sum_s 2^((m_s - M) c) O_s / sum_s 2^((m_s - M) c) l_s,  M = max_s m_s
+// (m_s in raw logit units, c = log2(e) / sqrt(d_h)), rounded once to bf16.
+// One block per item; thread t takes query t / 2, features 64 (t % 2) .. + 63.
+// ============================================================================
+__global__ __launch_bounds__(256) void xattn_merge(const float* __restrict__ partial, const XMerge* __restrict__ items,
+                                                   bf16* __restrict__ out, int ldo, float scale_log2) {
+  constexpr int DH = 128;
+  const XMerge it = items[blockIdx.x];
+  const int lq = threadIdx.x >> 1, half = threadIdx.x & 1;
+  if (lq >= it.q_count) return;
+  constexpr size_t kSlot = 128 * (DH + 2);
+  float M = -INFINITY;
+  for (int s = 0; s < it.n_parts; ++s) M = fmaxf(M, partial[(it.part0 + s) * kSlot + 128 * DH + lq]);
+  float acc[64];
+#pragma unroll
+  for (int e = 0; e < 64; ++e) acc[e] = 0.f;
+  float l = 0.f;
+  for (int s = 0; s < it.n_parts; ++s) {
+    const float* ps = partial + (it.part0 + s) * kSlot;
+    const float ms = ps[128 * DH + lq];
+    const float w = ms == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((ms - M) * scale_log2);
+    l = fmaf(w, ps[128 * DH + 128 + lq], l);
+    const floatx4* o = reinterpret_cast<const floatx4*>(ps + (size_t)lq * DH + 64 * half);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const floatx4 v = o[e];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) acc[4 * e + k] = fmaf(w, v[k], acc[4 * e + k]);
+    }
+  }
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  const int i = it.q_begin + lq;
+  const int row = i < it.qa_n ? it.qa_row + i : it.qb_row + (i - it.qa_n);
+  bf16* orow = out + (size_t)row * ldo + it.head * DH + 64 * half;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    bf16x8 v;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = (bf16)(acc[8 * e + k] * inv);
+    *reinterpret_cast<bf16x8*>(orow + 8 * e) = v;
+  }
+}
+
+bool cross_attention_split_ok(bool bf, int dh) { return bf && dh == 128; }
+
+hipError_t launch_cross_attention(const void* q, int ldq, void* out, int ldo, const void* pool,
+                                  const int32_t* page_table, int max_pages, PageGeom g, int layer_slot,
+                                  const XTile* tiles, const int32_t* xoff, int longest_list,
+                                  const XTile* split_tiles, const int32_t* split_xoff, int split_longest,
+                                  float* partial, const XMerge* merges, int n_merges, hipStream_t s) {
+  if (g.dh != 128) return hipErrorInvalidValue;
+  const float sl2 = kLog2e / sqrtf(128.f);
+  if (longest_list > 0)
+    paged_attn_mfma3<128, false><<<8 * longest_list, 256, 0, s>>>((const bf16*)q, ldq, (bf16*)out, ldo,
+                                                                   (const bf16*)pool, page_table, max_pages, g,
+                                                                   layer_slot, tiles, xoff, partial, sl2, 8.f / sl2);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || split_longest <= 0) return e;
+  paged_attn_mfma3<128, true><<<8 * split_longest, 256, 0, s>>>((const bf16*)q, ldq, (bf16*)out, ldo,
+                                                                 (const bf16*)pool, page_table, max_pages, g,
+                                                                 layer_slot, split_tiles, split_xoff, partial, sl2,
+                                                                 8.f / sl2);
+  e = hipGetLastError();
+  if (e != hipSuccess || n_merges <= 0) return e;
+  xattn_merge<<<n_merges, 256, 0, s>>>(partial, merges, (bf16*)out, ldo, sl2);
+  return hipGetLastError();
 }
 
 // ============================================================================
@@ -880,9 +990,7 @@ hipError_t launch_paged_attention(bool bf, const void* q, int ldq, void* out, in
       if (causal) TX_PA(64, true); else TX_PA(64, false);
     } else {
       if (causal) TX_PA(128, true);
-      else
-        paged_attn_mfma3<128><<<n_tiles, 256, 0, s>>>(qq, ldq, oo, ldo, pp, page_table, max_pages, g, layer_slot,
-                                                       reqs, tiles, sl2);
+      else TX_PA(128, false);
     }
 #undef TX_PA
     return hipGetLastError();

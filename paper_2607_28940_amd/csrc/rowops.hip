@@ -220,10 +220,19 @@ __global__ __launch_bounds__(256) void scatter_pages(const T* __restrict__ src, 
         *reinterpret_cast<const u32x4*>(ksrc + (size_t)t * lds + ch * VEC);
   }
   constexpr int RC = kPage / VEC;  // 16-byte pieces per V^T row
+  // A page tile that ends before the page does is its request's last: the
+  // columns of positions t1 .. 63 are set to zero, so that a kernel reading
+  // the whole page multiplies the masked keys' zero probabilities by zeros
+  // rather than by whatever the pool held there.
   if (n < kPage)
     for (int c = threadIdx.x; c < dh * RC; c += 256) {
       const int r = c / RC, q = c % RC;
-      *reinterpret_cast<u32x4*>(&sv[r * LDP + q * VEC]) = *reinterpret_cast<const u32x4*>(vdst + (size_t)r * kPage + q * VEC);
+      u32x4 raw = *reinterpret_cast<const u32x4*>(vdst + (size_t)r * kPage + q * VEC);
+      T* v = reinterpret_cast<T*>(&raw);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e)
+        if (vt_col(q * VEC + e) >= tl.t1) v[e] = (T)0.f;
+      *reinterpret_cast<u32x4*>(&sv[r * LDP + q * VEC]) = raw;
     }
   __syncthreads();
   for (int c = threadIdx.x; c < n * cpr; c += 256) {

@@ -18,6 +18,8 @@ typedef _Float16 f16;
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kPage = 64;  // tokens per cache page
 
@@ -43,6 +45,26 @@ struct AttnTile {
 // serving row and themselves).
 struct SelfReq {
   int32_t s_row, S, c_row, C;
+};
+
+// A tile of the decoder cross-attention: queries q_begin ..
+// q_begin + q_count - 1 (at most 128) of one request and head against the
+// request's key pages page_begin .. page_end - 1. Query i of the request lives
+// in activation row (i < qa_n ? qa_row + i : qb_row + i - qa_n); kv_len is the
+// request's cached length (keys past it, on its last page, are masked), slot
+// its page-table row. part < 0: the tile covers every page and writes the
+// output rows; part >= 0: a kv-split tile that writes its unnormalised output,
+// running max and sum to partial slot `part` (128 x (d_h + 2) floats).
+struct XTile {
+  int32_t head, q_begin, q_count, part;
+  int32_t page_begin, page_end, kv_len, slot;
+  int32_t qa_row, qa_n, qb_row, pad;
+};
+// Merge of the n_parts partial slots part0 .. part0 + n_parts - 1 of one
+// (request, head, query block) into its output rows.
+struct XMerge {
+  int32_t head, q_begin, q_count, part0;
+  int32_t n_parts, qa_row, qa_n, qb_row;
 };
 
 // Self-attention tile: queries q_begin.. (in the request's [serving; candidate]
@@ -187,6 +209,21 @@ hipError_t launch_lg_attention(bool bf, const void* q, int ldq, void* out, int l
                                const int32_t* page_table, int max_pages, PageGeom g, int layer_slot,
                                const AttnReq* reqs, const AttnTile* tiles, int n_tiles, int l_local,
                                const void* gkv, int gkv_ld, int dec_layer, hipStream_t s);
+// Decoder cross-attention over per-XCD tile lists (bf16, d_h = 128): XCD x
+// owns tiles[xoff[x] .. xoff[x + 1]); block b (which the hardware runs on XCD
+// b % 8) takes entry b / 8 of its XCD's list, on a grid of 8 x longest_list
+// blocks. The whole-request tiles write their rows; the kv-split tiles, a
+// tile set and a launch of their own, write partial slots (kXPartBytes
+// each), which the merge items then combine into the output rows.
+bool cross_attention_split_ok(bool bf, int dh);
+constexpr int kXQueryBlock = 128;  // queries per tile
+constexpr int kXBlocksPerCu = 3;   // resident blocks per CU
+constexpr size_t kXPartBytes = (size_t)128 * (128 + 2) * 4;  // one partial slot
+hipError_t launch_cross_attention(const void* q, int ldq, void* out, int ldo, const void* pool,
+                                  const int32_t* page_table, int max_pages, PageGeom g, int layer_slot,
+                                  const XTile* tiles, const int32_t* xoff, int longest_list,
+                                  const XTile* split_tiles, const int32_t* split_xoff, int split_longest,
+                                  float* partial, const XMerge* merges, int n_merges, hipStream_t s);
 constexpr int kLgQueryBlock = 64;
 constexpr int kMaxActions = 16;  // largest supported action vocabulary of the decoder head
 constexpr int kMaxLocal = 64;  // largest supported l_local

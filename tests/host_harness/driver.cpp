@@ -5,12 +5,14 @@
 // planning over many ragged requests and the failure path of a build or
 // append whose first HIP call fails after the pages were assigned (here:
 // the page-table upload, for want of a device).
+#include <algorithm>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <vector>
 
 #include "transx.h"
+#include "../../paper_2607_28940_amd/csrc/xplan.h"
 
 static int g_fail = 0;
 #define EXPECT(cond)                                                          \
@@ -38,7 +40,103 @@ static int64_t len_of(tx_kv_cache* c, int id) {
   return v;
 }
 
+
+// Properties of the cross-attention work list for one set of requests.
+// expect_split: 1 = some unit is split, 0 = none, -1 = either
+static void check_plan(const std::vector<tx::AttnReq>& reqs, int H, int blocks, int max_parts, int expect_split) {
+  tx::XPlan p;
+  tx::xattn_plan(reqs, H, blocks, max_parts, p);
+  EXPECT(p.n_parts <= max_parts);
+  // coverage[r][h][q][page]: how often the pair is computed
+  std::vector<std::vector<int>> cover(reqs.size() * H);
+  std::vector<int> part_use(p.n_parts, 0);
+  bool split = false;
+  for (int kind = 0; kind < 2; ++kind) {
+    const tx::XTileSet& set = kind ? p.split : p.whole;
+    EXPECT(set.xoff.size() == 9 && set.xoff[0] == 0 && set.xoff[8] == (int)set.tiles.size());
+    for (int x = 0; x < 8 && set.xoff.size() == 9; ++x) EXPECT(set.xoff[x] <= set.xoff[x + 1]);
+    int longest = 0;
+    for (int x = 0; x < 8 && set.xoff.size() == 9; ++x) longest = std::max(longest, set.xoff[x + 1] - set.xoff[x]);
+    EXPECT(set.longest() == longest);
+    for (const tx::XTile& t : set.tiles) {
+      int r = -1;
+      for (int i = 0; i < (int)reqs.size(); ++i)
+        if (reqs[i].slot == t.slot) r = i;
+      EXPECT(r >= 0);
+      if (r < 0) continue;
+      const tx::AttnReq& q = reqs[r];
+      const int nq = q.qa_n + q.qb_n, pages = (q.kv_len + 63) / 64;
+      EXPECT(t.head >= 0 && t.head < H && t.q_count >= 1 && t.q_count <= tx::kXQueryBlock);
+      EXPECT(t.q_begin >= 0 && t.q_begin + t.q_count <= nq && t.q_begin % tx::kXQueryBlock == 0);
+      EXPECT(t.page_begin >= 0 && t.page_begin < t.page_end && t.page_end <= pages);
+      EXPECT(t.kv_len == q.kv_len && t.qa_row == q.qa_row && t.qa_n == q.qa_n && t.qb_row == q.qb_row);
+      EXPECT((t.part >= 0) == (kind == 1));  // each kind in its own set
+      if (t.part >= 0) {
+        split = true;
+        EXPECT(t.part < p.n_parts);
+        if (t.part < p.n_parts) ++part_use[t.part];
+        EXPECT(t.page_end - t.page_begin >= tx::kXMinSplitPages);
+      } else {
+        EXPECT(t.page_begin == 0 && t.page_end == pages);
+      }
+      std::vector<int>& cv = cover[(size_t)r * H + t.head];
+      cv.resize((size_t)nq * pages, 0);
+      for (int i = t.q_begin; i < t.q_begin + t.q_count; ++i)
+        for (int pg = t.page_begin; pg < t.page_end; ++pg) ++cv[(size_t)i * pages + pg];
+    }
+  }
+  if (expect_split >= 0) EXPECT(split == (expect_split == 1));
+  for (int s = 0; s < p.n_parts; ++s) EXPECT(part_use[s] == 1);
+  for (int r = 0; r < (int)reqs.size(); ++r) {
+    const int nq = reqs[r].qa_n + reqs[r].qb_n, pages = (reqs[r].kv_len + 63) / 64;
+    for (int h = 0; h < H; ++h) {
+      const std::vector<int>& cv = cover[(size_t)r * H + h];
+      EXPECT(cv.size() == (size_t)nq * pages);
+      for (int v : cv) EXPECT(v == 1);
+    }
+  }
+  // merges: one per split (request, head, query block), covering its part slots
+  std::vector<int> merged(p.n_parts, 0);
+  for (const tx::XMerge& mg : p.merges) {
+    EXPECT(mg.n_parts >= 2 && mg.part0 >= 0 && mg.part0 + mg.n_parts <= p.n_parts);
+    for (int k = 0; k < mg.n_parts && mg.part0 + k < p.n_parts; ++k) ++merged[mg.part0 + k];
+  }
+  for (int s = 0; s < p.n_parts; ++s) EXPECT(merged[s] == 1);
+}
+
+static void check_plans() {
+  std::vector<tx::AttnReq> reqs;
+  // headline-like batch: no request is split
+  for (int r = 0; r < 64; ++r) reqs.push_back({r * 576, 64, 64 * 576 + r * 512, 512, 4096, 0, r, 0});
+  check_plan(reqs, 8, 512, 512, 0);
+  // four long requests with a ragged tail page: split, every part >= 16 pages
+  reqs.clear();
+  for (int r = 0; r < 4; ++r) reqs.push_back({r * 600, 64, 4 * 600 + r * 536, 536 + r, 16384 - 37 * r, 0, 10 + r, 0});
+  check_plan(reqs, 8, 512, 512, 1);
+  // the same with too few partial slots for any split: the quantum grows
+  // past the longest unit
+  check_plan(reqs, 8, 512, 40, 0);
+  // one long request, two heads, one query block: 32 slots suffice
+  reqs.assign(1, tx::AttnReq{0, 30, 30, 70, 16384, 0, 2, 0});
+  check_plan(reqs, 2, 512, 40, 1);
+  // one request, one head, one query, short cache: a single tile
+  reqs.assign(1, tx::AttnReq{5, 1, 0, 0, 100, 0, 3, 0});
+  check_plan(reqs, 1, 512, 512, 0);
+  // ragged mix, no candidates for some requests
+  reqs.clear();
+  uint32_t z = 12345;
+  auto rnd = [&](int n) { z = z * 1664525u + 1013904223u; return (int)((z >> 8) % (uint32_t)n); };
+  int row = 0;
+  for (int r = 0; r < 40; ++r) {
+    const int S = rnd(65), C = rnd(300), L = 1 + rnd(9000);
+    reqs.push_back({row, S, row + S, C, L, 0, r, 0});
+    row += S + C;
+  }
+  check_plan(reqs, 4, 64, 512, -1);
+}
+
 int main() {
+  check_plans();
   tx_config cfg = headline();
   const size_t rb = tx_model_repack_bytes(&cfg);
   EXPECT(rb > 0);

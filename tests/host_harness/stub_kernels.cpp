@@ -47,6 +47,12 @@ hipError_t launch_lg_attention(bool, const void*, int, void*, int, const void*, 
   return hipSuccess;
 }
 hipError_t static_scratch(void**) { return hipErrorNoDevice; }
+bool cross_attention_split_ok(bool bf, int dh) { return bf && dh == 128; }
+hipError_t launch_cross_attention(const void*, int, void*, int, const void*, const int32_t*, int, PageGeom, int,
+                                  const XTile*, const int32_t*, int, const XTile*, const int32_t*, int, float*,
+                                  const XMerge*, int, hipStream_t) {
+  return hipSuccess;
+}
 hipError_t launch_transpose(bool, const void*, void*, int, int, int, hipStream_t) { return hipSuccess; }
 hipError_t launch_transpose_to_f32(bool, const void*, float*, int, int, hipStream_t) { return hipSuccess; }
 hipError_t launch_to_f32(bool, const void*, float*, int64_t, hipStream_t) { return hipSuccess; }

@@ -64,6 +64,26 @@ def test_bf16_ragged_vs_oracle(O, name, model):
     _compare_all(run, O.Oracle(model, w), range(wl.B), BF16_TOL, f"bf16 ragged {name}")
 
 
+def test_kv_split_vs_oracle(O):
+    """Few requests with long caches: the cross-attention work list splits the
+    long request's pages over several tiles per (head, query block) and merges
+    their partial results (log-sum-exp), since a whole-request tile would leave
+    the GPU idle (3000 cached tokens = 47 pages, in parts of at least 16). The
+    scores match the oracle; reordering the candidates does not change the
+    plan, and every candidate's scores are bitwise unchanged."""
+    model = SMALL_BF16[0][1]
+    wl = I.custom_workload(model, cfg_id=37, L=[3000, 40], S=[5, 3], C=[200, 10])
+    w = I.make_weights(model, ("sharp", "affine"))
+    run = DeviceCase(wl, w)
+    run.build(range(wl.B))
+    _compare_all(run, O.Oracle(model, w), range(wl.B), BF16_TOL, "kv-split")
+    base = run.score([0, 1])
+    cand = [I.request_tokens(wl, r, I.STREAM_CANDIDATES)[::-1].copy() for r in range(wl.B)]
+    rev = run.score([0, 1], cand=cand)
+    for r in range(wl.B):
+        assert np.array_equal(rev[r], base[r][::-1]), r
+
+
 # Enough rows for the persistent GEMM (M >= 2048 encoder and decoder rows,
 # neither a multiple of its 256-row tile), at the smallest K it takes (256:
 # the QKV, attention-output and FFN-up projections of a d = 256 model) and at

@@ -21,6 +21,7 @@ def test_host_logic_under_sanitizers(tmp_path):
            "-Xarch_host", "-fno-sanitize-recover=undefined",
            "-I" + os.path.join(ROOT, "include"),
            os.path.join(ROOT, "paper_2607_28940_amd", "csrc", "api.cpp"),
+           os.path.join(ROOT, "paper_2607_28940_amd", "csrc", "xplan.cpp"),
            os.path.join(HARNESS, "stub_kernels.cpp"), os.path.join(HARNESS, "driver.cpp"), "-o", exe]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-4000:]
