@@ -1146,7 +1146,7 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
     mx = std::max<int64_t>(mx, S + C);
   }
   const bool sparse = m->l_local > 0;
-  const int qb = sparse ? kLgQueryBlock : paged_attention_q_block(bf, m->dh);
+  const int qb = sparse ? lg_attention_q_block(bf, m->l_local, m->gpool) : paged_attention_q_block(bf, m->dh);
   const int sqb = self_attention_q_block(bf, m->dh);
   std::vector<AttnTile> t_full, t_cand;
   std::vector<SelfTile> s_full, s_cand;
@@ -1278,7 +1278,7 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
               launch_gemm(bf, T + ro, d, L.xq.w, L.xq.b, nullptr, 0, A + ro, d, Mr, d, d, EPI_BIAS, st));
     TX_LAUNCH(K_CROSS_ATTN, 4 * dd * (last ? pairs_cand : pairs_full), kvb + 2 * Mrd * dd * esd,
               sparse ? launch_lg_attention(bf, A, d, O, d, c->pool, c->d_table, c->max_pages, c->geom, m->n_enc + l,
-                                           areq, at, n_at, m->l_local, m->gpool ? c->d_gkv : nullptr,
+                                           areq, at, n_at, qb, m->l_local, m->gpool ? c->d_gkv : nullptr,
                                            2 * m->n_dec * d, l, st)
               : xpipe ? launch_cross_attention(
                             A, d, O, d, c->pool, c->d_table, c->max_pages, c->geom, m->n_enc + l,

@@ -211,13 +211,196 @@ __global__ __launch_bounds__(256) void lg_cross_attn(const T* __restrict__ q, in
   for (int e = 0; e < DP; ++e) out[(size_t)row * ldo + h * DH + part * DP + e] = (T)(acc[e] * inv);
 }
 
+// bf16 models with at most 16 keys per query (l_local <= 15 with the global
+// token, l_local <= 16 without; the paper's setting is 10 + 1): the keys and
+// values stay bf16 in LDS and both products run on v_dot2_f32_bf16 (two
+// bf16 products per instruction, fp32 accumulation). Four lanes serve a
+// query; lane `part` owns the 8-feature pieces part, part + 4, ... of the
+// head, so each 16-byte load or store of Q and O covers 64 contiguous bytes
+// of a row per query. The query's Q pieces are requested before the block
+// stages its keys, so their latency overlaps the staging.
+// Keys are staged in slots of pairs aligned to even cache positions: pair a
+// holds positions 2 (a0 + a) and 2 (a0 + a) + 1, which sit side by side in a
+// page's V^T slab (the slab's column permutation keeps even-odd neighbours
+// together), so one 4-byte load fetches both values of a feature. Window
+// positions below k0 or at len and above are masked (their K rows are zero in
+// LDS; a V value at len is the zero the page scatter keeps past a request's
+// length, and the one below k0 is a valid cached value times probability 0).
+// The pooled token takes the pair after the window, with a zero partner. All
+// of a query's scores are formed first (in registers), then the softmax, then
+// PV over the pairs, one dot2 per pair and feature, with the probabilities
+// rounded to bf16 (as the dense kernels round P) and l summed over the
+// rounded values.
+constexpr int kLgDotKeys = 16;
+constexpr int kLgDotQueries = 128;  // queries per block (4 lanes each)
+constexpr int kLgQueries = 64;      // queries per block of the general kernel
+constexpr int kLgDotPairs = kLgDotKeys / 2 + 2;  // window + alignment + pooled token
+
+template <int DH>
+__global__ __launch_bounds__(4 * kLgDotQueries) void lg_cross_attn_dot(const bf16* __restrict__ q, int ldq, bf16* __restrict__ out,
+                                                         int ldo, const bf16* __restrict__ pool,
+                                                         const int32_t* __restrict__ page_table, int max_pages,
+                                                         PageGeom g, int layer_slot, const AttnReq* __restrict__ reqs,
+                                                         const AttnTile* __restrict__ tiles, int l_local,
+                                                         const bf16* __restrict__ gkv, int gkv_ld, int dec_layer,
+                                                         float scale_log2) {
+  constexpr int NP = DH / 32;  // pieces per lane
+  constexpr int MP = kLgDotPairs, MS = 2 * MP;
+  __shared__ __attribute__((aligned(16))) bf16 sK[MS * DH];
+  __shared__ __attribute__((aligned(16))) uint32_t sV[MP * DH];
+  const AttnTile tile = tiles[blockIdx.x];
+  if (tile.q_count <= 0) return;
+  const AttnReq rq = reqs[tile.req];
+  const int h = tile.head, tid = threadIdx.x, qi = tid >> 2, part = tid & 3;
+  const bool active = qi < tile.q_count;
+  // the query's Q pieces, requested first
+  bf16x8 qv[NP];
+  int row = 0;
+  if (active) {
+    const int i = tile.q_begin + qi;
+    row = i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
+#pragma unroll
+    for (int e = 0; e < NP; ++e)
+      qv[e] = *reinterpret_cast<const bf16x8*>(q + (size_t)row * ldq + h * DH + (e * 4 + part) * 8);
+  }
+  const int len = rq.kv_len;
+  const int k0 = max(0, len - l_local);
+  const int a0 = k0 >> 1, npl = ((len - 1) >> 1) - a0 + 1;  // local pairs
+  const int np = npl + (gkv ? 1 : 0);
+  const int p0 = 2 * a0;  // position of slot 0
+  // the window's (at most two) pages, as scalars
+  const int32_t* ptab = page_table + (size_t)rq.slot * max_pages;
+  const int pg_lo = p0 / kPage, pg_hi = (2 * (a0 + npl) - 1) / kPage;
+  const bf16* page_lo = pool + (size_t)ptab[pg_lo] * g.page_elems;
+  const bf16* page_hi = pool + (size_t)ptab[pg_hi] * g.page_elems;
+  const int d = g.H * DH;
+  const bf16* gk = gkv ? gkv + (size_t)rq.slot * gkv_ld + (size_t)(2 * dec_layer) * d + h * DH : nullptr;
+  // K rows of every slot, 16 bytes per thread and step
+  for (int e = tid; e < 2 * np * (DH / 8); e += 4 * kLgDotQueries) {
+    const int j = e / (DH / 8), c = e % (DH / 8);
+    bf16x8 v = {};
+    if (j < 2 * npl) {
+      const int pos = p0 + j;
+      if (pos >= k0 && pos < len) {
+        const bf16* pg = pos / kPage == pg_lo ? page_lo : page_hi;
+        v = *reinterpret_cast<const bf16x8*>(pg + g.k_off(layer_slot, h) + (size_t)(pos % kPage) * DH + c * 8);
+      }
+    } else if (j == 2 * npl) {
+      v = *reinterpret_cast<const bf16x8*>(gk + c * 8);
+    }
+    *reinterpret_cast<bf16x8*>(sK + j * DH + c * 8) = v;
+  }
+  // V pairs: one 4-byte word of the V^T slab per pair and feature
+  for (int e = tid; e < np * DH; e += 4 * kLgDotQueries) {
+    const int a = e / DH, f = e % DH;
+    uint32_t w;
+    if (a < npl) {
+      const int pos = p0 + 2 * a;
+      const bf16* pg = pos / kPage == pg_lo ? page_lo : page_hi;
+      w = *reinterpret_cast<const uint32_t*>(pg + g.v_off(layer_slot, h) + (size_t)f * kPage + vt_col(pos % kPage));
+    } else {
+      const bf16x2 v2 = {gk[d + f], (bf16)0.f};
+      w = __builtin_bit_cast(uint32_t, v2);
+    }
+    sV[a * DH + f] = w;
+  }
+  __syncthreads();
+  if (!active) return;
+  // slot j is a key unless it lies outside the window (slot 0 below k0, the
+  // window's last slot at len) or is the pooled token's zero partner
+  auto is_key = [&](int j) {
+    if (j >= 2 * np) return false;
+    if (j < 2 * npl) return p0 + j >= k0 && p0 + j < len;
+    return j == 2 * npl;
+  };
+  float s[MS];
+  float m = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < MS; ++j) {
+    s[j] = -INFINITY;
+    if (is_key(j)) {
+      float acc = 0.f;
+#pragma unroll
+      for (int e = 0; e < NP; ++e) {
+        const bf16x8 k8 = *reinterpret_cast<const bf16x8*>(sK + j * DH + (e * 4 + part) * 8);
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{qv[e][2 * c], qv[e][2 * c + 1]},
+                                                bf16x2{k8[2 * c], k8[2 * c + 1]}, acc, false);
+      }
+      s[j] = quad_sum(acc) * scale_log2;
+      m = fmaxf(m, s[j]);
+    }
+  }
+  bf16 pb[MS];
+  float l = 0.f;
+#pragma unroll
+  for (int j = 0; j < MS; ++j) {
+    pb[j] = (bf16)__builtin_amdgcn_exp2f(s[j] - m);  // 0 where masked
+    l += (float)pb[j];
+  }
+  float o[NP][8];
+#pragma unroll
+  for (int e = 0; e < NP; ++e)
+#pragma unroll
+    for (int c = 0; c < 8; ++c) o[e][c] = 0.f;
+#pragma unroll
+  for (int a = 0; a < MP; ++a) {
+    if (a < np) {
+      const bf16x2 pp = {pb[2 * a], pb[2 * a + 1]};
+#pragma unroll
+      for (int e = 0; e < NP; ++e) {
+        // features (e * 4 + part) * 8 .. + 7 of the pair, 16 bytes per 4 features
+        // (taken apart element-wise: this compiler folds a bit_cast of u32
+        // vector element c to element 0)
+        const bf16* vr = reinterpret_cast<const bf16*>(sV + a * DH + (e * 4 + part) * 8);
+        const bf16x8 v0 = *reinterpret_cast<const bf16x8*>(vr);
+        const bf16x8 v1 = *reinterpret_cast<const bf16x8*>(vr + 8);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          o[e][c] = __builtin_amdgcn_fdot2_f32_bf16(pp, bf16x2{v0[2 * c], v0[2 * c + 1]}, o[e][c], false);
+          o[e][4 + c] = __builtin_amdgcn_fdot2_f32_bf16(pp, bf16x2{v1[2 * c], v1[2 * c + 1]}, o[e][4 + c], false);
+        }
+      }
+    }
+  }
+  const float inv = 1.f / l;
+#pragma unroll
+  for (int e = 0; e < NP; ++e) {
+    bf16x8 w;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) w[c] = (bf16)(o[e][c] * inv);
+    *reinterpret_cast<bf16x8*>(out + (size_t)row * ldo + h * DH + (e * 4 + part) * 8) = w;
+  }
+}
+
+static bool lg_dot_path(bool bf, int l_local, bool gpool) { return bf && l_local + (gpool ? 1 : 0) <= kLgDotKeys; }
+int lg_attention_q_block(bool bf, int l_local, bool gpool) {
+  return lg_dot_path(bf, l_local, gpool) ? kLgDotQueries : kLgQueries;
+}
+
 hipError_t launch_lg_attention(bool bf, const void* q, int ldq, void* out, int ldo, const void* pool,
                                const int32_t* page_table, int max_pages, PageGeom g, int layer_slot,
-                               const AttnReq* reqs, const AttnTile* tiles, int n_tiles, int l_local,
+                               const AttnReq* reqs, const AttnTile* tiles, int n_tiles, int q_block, int l_local,
                                const void* gkv, int gkv_ld, int dec_layer, hipStream_t s) {
   if (n_tiles <= 0) return hipSuccess;
   if (l_local < 1 || l_local > kMaxLocal) return hipErrorInvalidValue;
+  if (q_block != lg_attention_q_block(bf, l_local, gkv != nullptr)) return hipErrorInvalidValue;
   const float sl2 = 1.4426950408889634f / sqrtf((float)g.dh);
+  if (lg_dot_path(bf, l_local, gkv != nullptr)) {
+#define TX_LGD(DH)                                                                                             \
+  lg_cross_attn_dot<DH><<<n_tiles, 4 * kLgDotQueries, 0, s>>>((const bf16*)q, ldq, (bf16*)out, ldo, (const bf16*)pool,      \
+                                                page_table, max_pages, g, layer_slot, reqs, tiles, l_local,    \
+                                                (const bf16*)gkv, gkv_ld, dec_layer, sl2)
+    switch (g.dh) {
+      case 32: TX_LGD(32); break;
+      case 64: TX_LGD(64); break;
+      case 128: TX_LGD(128); break;
+      default: return hipErrorInvalidValue;
+    }
+#undef TX_LGD
+    return hipGetLastError();
+  }
   const size_t lds = (size_t)(l_local + 1) * 4 * (g.dh / 4 + 4) * 2 * sizeof(float);
 #define TX_LG(TT, DH)                                                                                            \
   lg_cross_attn<TT, DH><<<n_tiles, 256, lds, s>>>((const TT*)q, ldq, (TT*)out, ldo, (const TT*)pool, page_table, \

@@ -11,6 +11,7 @@ namespace tx {
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 // Storage of a post-LN sublayer's pre-LayerNorm sum (bias + residual +
 // sublayer output) in bf16 models: 11 mantissa bits at the width of bf16.
@@ -203,11 +204,12 @@ hipError_t launch_store_rows(bool bf, const void* src, int W, const PoolReq* req
 // min(l_local, kv_len) cached tokens of its request (layer slot layer_slot)
 // and, when gkv is not null, to the request's global token, whose key and
 // value are columns [2*dec_layer*d + h*dh ..) and [(2*dec_layer+1)*d + h*dh ..)
-// of row `slot` of gkv (row stride gkv_ld). Tiles of lg_attention_q_block()
-// queries.
+// of row `slot` of gkv (row stride gkv_ld). Tiles of q_block =
+// lg_attention_q_block(bf, l_local, gkv != nullptr) queries (checked).
+int lg_attention_q_block(bool bf, int l_local, bool gpool);
 hipError_t launch_lg_attention(bool bf, const void* q, int ldq, void* out, int ldo, const void* pool,
                                const int32_t* page_table, int max_pages, PageGeom g, int layer_slot,
-                               const AttnReq* reqs, const AttnTile* tiles, int n_tiles, int l_local,
+                               const AttnReq* reqs, const AttnTile* tiles, int n_tiles, int q_block, int l_local,
                                const void* gkv, int gkv_ld, int dec_layer, hipStream_t s);
 // Decoder cross-attention over per-XCD tile lists (bf16, d_h = 128): XCD x
 // owns tiles[xoff[x] .. xoff[x + 1]); block b (which the hardware runs on XCD
@@ -224,7 +226,6 @@ hipError_t launch_cross_attention(const void* q, int ldq, void* out, int ldo, co
                                   const XTile* tiles, const int32_t* xoff, int longest_list,
                                   const XTile* split_tiles, const int32_t* split_xoff, int split_longest,
                                   float* partial, const XMerge* merges, int n_merges, hipStream_t s);
-constexpr int kLgQueryBlock = 64;
 constexpr int kMaxActions = 16;  // largest supported action vocabulary of the decoder head
 constexpr int kMaxLocal = 64;  // largest supported l_local
 
