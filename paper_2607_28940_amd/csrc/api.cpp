@@ -80,9 +80,20 @@ struct EncLayer {
   Mat qkv, o, f1, f2;
   float *ln1g, *ln1b, *ln2g, *ln2b, *rel;
 };
+// A consumer GEMM with the preceding LayerNorm folded in (bf16 models, see
+// EPI_LN in tx_internal.h): gain-scaled weight [N][K] in fp16, its column sums
+// and the bias with the LayerNorm offset folded in.
+struct Fold {
+  void* w = nullptr;
+  float* cs = nullptr;
+  float* b = nullptr;
+};
 struct DecLayer {
   Mat qkv, o, xq, xo, f1, f2;
   float *ln1g, *ln1b, *ln2g, *ln2b, *ln3g, *ln3b;
+  // cross-Q with LN1, FFN up with LN2, and (layers after the first) QKV with
+  // the previous layer's LN3 folded in
+  Fold xqf, f1f, qkvf;
 };
 enum { E_WQ, E_BQ, E_WK, E_BK, E_WV, E_BV, E_WO, E_BO, E_LN1G, E_LN1B, E_W1, E_B1, E_W2, E_B2, E_LN2G, E_LN2B,
        E_REL, E_N };
@@ -106,6 +117,8 @@ struct tx_model {
   bool gpool = false;      // the sparse key set includes the pooled global token
   int n_act = 0;           // 0: scalar logit head (ws [d], bs [1]); k: ws [k][d], bs [k]
   bool weights_set = false;
+  bool ln_fold = false;    // bf16: the folded weights exist and are finite in fp16
+  int* fold_flag = nullptr;  // device word: a folded weight overflowed fp16
 };
 
 static int check_config(const tx_config* c) {
@@ -151,8 +164,16 @@ static void layout_model(const tx_config& c, Carver& cv, tx_model& m) {
     L.ln1g = vec(d), L.ln1b = vec(d), L.ln2g = vec(d), L.ln2b = vec(d);
     L.rel = vec((size_t)H * R);
   }
+  auto fold = [&](int N, int K) {
+    Fold x;
+    x.w = cv.take<void*>((size_t)N * K * 2);
+    x.cs = vec(N);
+    x.b = vec(N);
+    return x;
+  };
   m.dec.resize(c.n_dec_layers);
-  for (auto& L : m.dec) {
+  for (int l = 0; l < c.n_dec_layers; ++l) {
+    DecLayer& L = m.dec[l];
     L.qkv = mat(3 * d, d);
     L.o = mat(d, d);
     L.xq = mat(d, d);
@@ -160,7 +181,13 @@ static void layout_model(const tx_config& c, Carver& cv, tx_model& m) {
     L.f1 = mat(F, d);
     L.f2 = mat(d, F);
     L.ln1g = vec(d), L.ln1b = vec(d), L.ln2g = vec(d), L.ln2b = vec(d), L.ln3g = vec(d), L.ln3b = vec(d);
+    if (c.dtype == TX_BF16) {
+      L.xqf = fold(d, d);
+      L.f1f = fold(F, d);
+      if (l > 0) L.qkvf = fold(3 * d, d);
+    }
   }
+  if (c.dtype == TX_BF16) m.fold_flag = cv.take<int*>(sizeof(int));
   m.xkv = mat(2 * d * c.n_dec_layers, d);
   const int k = std::max(1, c.n_actions);
   m.ws = vec((size_t)d * k);
@@ -290,7 +317,27 @@ int tx_model_set_weights(tx_model* m, const void* const* W, int32_t n_weights, h
   else run(bias(hb, m->ws, d));
   run(bias(hb + 1, m->bs, k));
   if (m->gpool) run(bias(hb + 2, m->wpool, d));
+  // the LayerNorm folds of the bf16 score pass; they stay unused when a
+  // gain-scaled weight does not fit fp16 (read back once, here)
+  m->ln_fold = false;
+  if (bf) {
+    run(launch_zero_int(m->fold_flag, stream));
+    for (int l = 0; l < m->n_dec; ++l) {
+      DecLayer& L = m->dec[l];
+      run(launch_fold_ln_weight(L.xq.w, d, d, L.ln1g, L.ln1b, L.xq.b, L.xqf.w, L.xqf.cs, L.xqf.b, m->fold_flag, stream));
+      run(launch_fold_ln_weight(L.f1.w, F, d, L.ln2g, L.ln2b, L.f1.b, L.f1f.w, L.f1f.cs, L.f1f.b, m->fold_flag, stream));
+      if (l > 0)
+        run(launch_fold_ln_weight(L.qkv.w, 3 * d, d, m->dec[l - 1].ln3g, m->dec[l - 1].ln3b, L.qkv.b, L.qkvf.w,
+                                  L.qkvf.cs, L.qkvf.b, m->fold_flag, stream));
+    }
+  }
   if (e != hipSuccess) return fail(TX_E_HIP, "weight repack launch failed: %s", hipGetErrorString(e));
+  if (bf) {
+    int flag = 1;
+    e = read_int(m->fold_flag, &flag, stream);
+    if (e != hipSuccess) return fail(TX_E_HIP, "weight fold check failed: %s", hipGetErrorString(e));
+    m->ln_fold = flag == 0;
+  }
   m->weights_set = true;
   return TX_OK;
 }
@@ -1246,9 +1293,20 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
     auto Yk = [&](int k) { return Ys[k & 1] + ro; };
     auto Sk = [&](int k) { return Ss[k & 1] + r0; };
     const int k0 = 3 * l;
+    // LayerNorm folds (bf16): the LayerNorms before the cross-Q and FFN-up
+    // GEMMs (rows r0 ..) and before the next layer's QKV GEMM (all rows) write
+    // only their row statistics, and those GEMMs multiply the stored pre-LN
+    // sums by the gain-scaled weights (EPI_LN); T is then not written at all
+    // (a model-level choice: a score does not depend on the batch it is in)
+    const bool fold = m->ln_fold && gemm_ln_ok(d, d, d, d) && gemm_ln_ok(F, d, d, F);
+    const bool fold_qkv = m->ln_fold && gemm_ln_ok(3 * d, d, d, 3 * d);
+    const bool fold_in = l > 0 && fold_qkv, fold_out = !last && fold_qkv;
     // layer input rows r0 .. M - 1: T, or the token arrays in place (first layer)
     const bool in_place = l == 0 && direct;
     TX_LAUNCH(K_GEMM_QKV, q.first, q.second, [&]() -> hipError_t {
+      if (fold_in)
+        return launch_gemm(bf, Ys[(k0 - 1) & 1], d, L.qkvf.w, L.qkvf.b, nullptr, 0, QKV, 3 * d, M, 3 * d, d, EPI_LN,
+                           st, LnResid{Ss[(k0 - 1) & 1], L.qkvf.cs, nullptr});
       if (!in_place) return launch_gemm(bf, T, d, L.qkv.w, L.qkv.b, nullptr, 0, QKV, 3 * d, M, 3 * d, d, EPI_BIAS, st);
       hipError_t e = launch_gemm(bf, Xs, d, L.qkv.w, L.qkv.b, nullptr, 0, QKV, 3 * d, (int)Ms, 3 * d, d, EPI_BIAS, st);
       if (e != hipSuccess) return e;
@@ -1272,10 +1330,12 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
       }
       return launch_gemm(bf, A + cs, d, L.o.w, L.o.b, Xc, d, Ys[0] + cs, d, (int)Mc, d, d, EPI_BIAS_RESID, st);
     }());
-    TX_LAUNCH(K_LAYERNORM, 0, 2 * Mrd * dd * esd,
-              launch_layernorm(bf, Yk(k0), T + ro, Sk(k0), L.ln1g, L.ln1b, Mr, d, eps, st));
+    TX_LAUNCH(K_LAYERNORM, 0, (fold ? 1 : 2) * Mrd * dd * esd,
+              launch_layernorm(bf, Yk(k0), fold ? nullptr : T + ro, Sk(k0), L.ln1g, L.ln1b, Mr, d, eps, st));
     TX_LAUNCH(K_GEMM_XQ, xq.first, xq.second,
-              launch_gemm(bf, T + ro, d, L.xq.w, L.xq.b, nullptr, 0, A + ro, d, Mr, d, d, EPI_BIAS, st));
+              fold ? launch_gemm(bf, Yk(k0), d, L.xqf.w, L.xqf.b, nullptr, 0, A + ro, d, Mr, d, d, EPI_LN, st,
+                                 LnResid{Sk(k0), L.xqf.cs, nullptr})
+                   : launch_gemm(bf, T + ro, d, L.xq.w, L.xq.b, nullptr, 0, A + ro, d, Mr, d, d, EPI_BIAS, st));
     TX_LAUNCH(K_CROSS_ATTN, 4 * dd * (last ? pairs_cand : pairs_full), kvb + 2 * Mrd * dd * esd,
               sparse ? launch_lg_attention(bf, A, d, O, d, c->pool, c->d_table, c->max_pages, c->geom, m->n_enc + l,
                                            areq, at, n_at, qb, m->l_local, m->gpool ? c->d_gkv : nullptr,
@@ -1290,11 +1350,13 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
     TX_LAUNCH(K_GEMM_XO, xo.first, xo.second,
               launch_gemm(bf, O + ro, d, L.xo.w, L.xo.b, Yk(k0), d, Yk(k0 + 1), d, Mr, d, d, EPI_BIAS_RESLN, st,
                           LnResid{Sk(k0), L.ln1g, L.ln1b}));
-    TX_LAUNCH(K_LAYERNORM, 0, 2 * Mrd * dd * esd,
-              launch_layernorm(bf, Yk(k0 + 1), T + ro, Sk(k0 + 1), L.ln2g, L.ln2b, Mr, d, eps, st));
+    TX_LAUNCH(K_LAYERNORM, 0, (fold ? 1 : 2) * Mrd * dd * esd,
+              launch_layernorm(bf, Yk(k0 + 1), fold ? nullptr : T + ro, Sk(k0 + 1), L.ln2g, L.ln2b, Mr, d, eps, st));
     TX_LAUNCH(K_GEMM_FFN1, f1.first, f1.second,
-              launch_gemm(bf, T + ro, d, L.f1.w, L.f1.b, nullptr, 0, Hf + (size_t)r0 * F * es, F, Mr, F, d,
-                          EPI_BIAS_GELU, st));
+              fold ? launch_gemm(bf, Yk(k0 + 1), d, L.f1f.w, L.f1f.b, nullptr, 0, Hf + (size_t)r0 * F * es, F, Mr, F,
+                                 d, EPI_LN_GELU, st, LnResid{Sk(k0 + 1), L.f1f.cs, nullptr})
+                   : launch_gemm(bf, T + ro, d, L.f1.w, L.f1.b, nullptr, 0, Hf + (size_t)r0 * F * es, F, Mr, F, d,
+                                 EPI_BIAS_GELU, st));
     TX_LAUNCH(K_GEMM_FFN2, f2.first, f2.second,
               launch_gemm(bf, Hf + (size_t)r0 * F * es, F, L.f2.w, L.f2.b, Yk(k0 + 1), d, Yk(k0 + 2), d, Mr, d, F,
                           EPI_BIAS_RESLN, st, LnResid{Sk(k0 + 1), L.ln2g, L.ln2b}));
@@ -1305,8 +1367,9 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
                                        d, eps, m->n_act, st));
     }
     else
-      TX_LAUNCH(K_LAYERNORM, 0, 2 * Mrd * dd * esd,
-                launch_layernorm(bf, Yk(k0 + 2), T + ro, Sk(k0 + 2), L.ln3g, L.ln3b, Mr, d, eps, st));
+      TX_LAUNCH(K_LAYERNORM, 0, (fold_out ? 1 : 2) * Mrd * dd * esd,
+                launch_layernorm(bf, Yk(k0 + 2), fold_out ? nullptr : T + ro, Sk(k0 + 2), L.ln3g, L.ln3b, Mr, d,
+                                 eps, st));
   }
   return TX_OK;
 }

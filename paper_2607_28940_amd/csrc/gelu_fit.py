@@ -13,7 +13,7 @@ Run: python3 gelu_fit.py  (prints the constants in the kernel's order).
 import numpy as np
 from scipy.special import erfc
 
-DEGREE = 7
+DEGREE = 5
 Z_MAX = 10.0
 NODES = 400
 LOG2E = 1.4426950408889634

@@ -31,22 +31,20 @@ namespace tx {
 // GELU(x) = x Phi(x) = max(x, 0) - u Phi(-u) with u = |x|, for either sign
 // of x. Phi(-u) = erfc(u / sqrt 2) / 2, with erfc(z) = t exp(-z^2 + P(t)),
 // t = 1 / (1 + z / 2) (the form of Press et al., Numerical Recipes erfcc) and
-// P a degree-7 least-squares fit on Chebyshev nodes (gelu_fit.py; fractional
-// error below 7.4e-7 for every argument, so the negative tail keeps its
-// relative accuracy). Evaluated as Phi(-u) = t 2^(P'(t) - (c u)^2) with
-// P' = log2(e) P - 1 and c^2 = log2(e) / 2: one reciprocal, one exp2 and 10
-// FMA-type operations.
+// P a degree-5 least-squares fit on Chebyshev nodes (gelu_fit.py; fractional
+// error below 8.2e-6 for every argument, 240 times below the bf16 output's
+// half unit, so the negative tail keeps its relative accuracy). Evaluated as
+// Phi(-u) = t 2^(P'(t) - (c u)^2) with P' = log2(e) P - 1 and
+// c^2 = log2(e) / 2: one reciprocal, one exp2 and 8 FMA-type operations.
 __device__ __forceinline__ float gelu_erf(float x) {
   const float u = fabsf(x);
   const float t = __builtin_amdgcn_rcpf(fmaf(u, 0.35355339059327373f, 1.0f));
-  float p = -0.2718776930163839f;
-  p = fmaf(p, t, 1.0879713150078754f);
-  p = fmaf(p, t, -1.449840280957486f);
-  p = fmaf(p, t, 0.5090884597583125f);
-  p = fmaf(p, t, -0.05895698505211376f);
-  p = fmaf(p, t, 0.5686708691445311f);
-  p = fmaf(p, t, 1.4406420004433174f);
-  p = fmaf(p, t, -2.825698746517148f);
+  float p = 0.3326649105748337f;
+  p = fmaf(p, t, -1.0313045036556072f);
+  p = fmaf(p, t, 0.694324586103557f);
+  p = fmaf(p, t, 0.3615738712795434f);
+  p = fmaf(p, t, 1.47012404965216f);
+  p = fmaf(p, t, -2.8273710833510295f);
   const float w = u * 0.8493218002880191f;
   const float q = t * __builtin_amdgcn_exp2f(fmaf(-w, w, p));  // Phi(-u)
   return fmaf(-u, q, fmaxf(x, 0.f));
@@ -56,8 +54,8 @@ template <int EPI>
 __device__ __forceinline__ float epilogue(float acc, float bias, float resid) {
 #pragma clang fp contract(off)
   float v = acc + bias;
-  if (EPI == EPI_BIAS_GELU) v = gelu_erf(v);
-  if (EPI >= EPI_BIAS_RESID) v += resid;
+  if (epi_gelu(EPI)) v = gelu_erf(v);
+  if (epi_resid(EPI)) v += resid;
   return v;
 }
 
@@ -152,7 +150,13 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_mfma(const bf16* __restrict_
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[i], fx[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < 2; ++j) {
+          if (epi_lnfold(EPI))  // fp16 operands (see gemm_bf16_p4)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, fw[i]),
+                                                               __builtin_bit_cast(f16x8, fx[j]), acc[i][j], 0, 0, 0);
+          else
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[i], fx[j], acc[i][j], 0, 0, 0);
+        }
     }
     if (kt + 1 < nk) lstore(cur ^ 1);
     __syncthreads();
@@ -165,14 +169,25 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_mfma(const bf16* __restrict_
     const int m = m0 + wm * 64 + j * 32 + l32;
     if (m >= M) continue;
     LnRow st{0.f, 0.f};
-    if (EPI == EPI_BIAS_RESLN) st = ln.stats[m];
+    if (EPI == EPI_BIAS_RESLN || epi_lnfold(EPI)) st = ln.stats[m];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int n = n0 + wn * 64 + i * 32 + 8 * g + 4 * hi;
         floatx4 b4 = *reinterpret_cast<const floatx4*>(bias + n);
-        if (EPI >= EPI_BIAS_RESID) {
+        if (epi_lnfold(EPI)) {
+          // the same operations as the persistent kernel's epilogue
+          const floatx4 cs4 = *reinterpret_cast<const floatx4*>(ln.g + n);
+          bf16x4 o;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            float v = fmaf(acc[i][j][4 * g + q], st.x, fmaf(st.y, cs4[q], b4[q]));
+            if (epi_gelu(EPI)) v = gelu_erf(v);
+            o[q] = (bf16)v;
+          }
+          *reinterpret_cast<bf16x4*>((bf16*)C + (size_t)m * ldc + n) = o;
+        } else if (epi_resid(EPI)) {
           const u32x2 raw = *reinterpret_cast<const u32x2*>((const bf16*)R + (size_t)m * ldr + n);
           floatx4 g4 = {0.f, 0.f, 0.f, 0.f};
           if (EPI == EPI_BIAS_RESLN) {
@@ -302,13 +317,21 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
 
   floatx16 acc[4][4];
   bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
+  // the LayerNorm-folding epilogues take fp16 operands (the stored pre-LN sum
+  // and the gain-scaled weight); the fragments are the same 16-byte units
   auto mfma16 = [&](auto Z_, const bf16x8(&fa)[4], const bf16x8(&fb)[4]) {
     constexpr bool Z = decltype(Z_)::value;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[i], fa[j], Z ? floatx16{} : acc[i][j], 0, 0, 0);
+      for (int j = 0; j < 4; ++j) {
+        if (epi_lnfold(EPI))
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, fb[i]),
+                                                             __builtin_bit_cast(f16x8, fa[j]),
+                                                             Z ? floatx16{} : acc[i][j], 0, 0, 0);
+        else
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[i], fa[j], Z ? floatx16{} : acc[i][j], 0, 0, 0);
+      }
   };
   using F0 = std::false_type;
   using T1 = std::true_type;
@@ -401,17 +424,18 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
   const int er = lane >> 3, ec = lane & 7;  // row (plus 8 u) and 8-float chunk of the read-back
   // epilogue resources (extents in bytes, below 2^32: checked by the launcher)
   // and the lane's fixed offsets: row wm * 128 + er (+ 32 j + 8 u), column
-  // wn * 128 + 8 ec (+ 64 h) of the tile; LayerNorm statistics of row wm * 128
-  // + l32 (+ 32 j)
+  // wn * 128 + 8 ec (+ 64 h) of the tile, and the LayerNorm statistics of the
+  // same rows
+  constexpr bool kStats = EPI == EPI_BIAS_RESLN || epi_lnfold(EPI);  // row statistics used
   const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)R, 0, EPI >= EPI_BIAS_RESID ? (int)(2u * (uint32_t)M * (uint32_t)ldr) : 0, 0x00020000);
+      (void*)R, 0, epi_resid(EPI) ? (int)(2u * (uint32_t)M * (uint32_t)ldr) : 0, 0x00020000);
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)ln.stats, 0, EPI == EPI_BIAS_RESLN ? (int)(8u * (uint32_t)M) : 0, 0x00020000);
+      (void*)ln.stats, 0, kStats ? (int)(8u * (uint32_t)M) : 0, 0x00020000);
   const __amdgpu_buffer_rsrc_t rc =
       __builtin_amdgcn_make_buffer_rsrc(C, 0, (int)(2u * (uint32_t)M * (uint32_t)ldc), 0x00020000);
   const uint32_t lr = 2u * (uint32_t)((wm * 128 + er) * ldr + wn * 128 + ec * 8);
   const uint32_t lc = 2u * (uint32_t)((wm * 128 + er) * ldc + wn * 128 + ec * 8);
-  const uint32_t ls = 8u * (uint32_t)(wm * 128 + l32);
+  const uint32_t ls = 8u * (uint32_t)(wm * 128 + er);
 
   for (int i = 0; i < my_tiles; ++i) {
     // the tile's first MFMAs take a zero accumulator input
@@ -432,27 +456,31 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
     // bias, GELU or residual applied with one rounding (bf16, or fp16 for a
     // pre-LN sum). Rows past M (computed from zero rows) are not stored.
     // Rounds (j, h): 32 rows (32 j ..) x 64 columns (64 h ..) of the wave's
-    // 128 x 128. The residual pieces of a round are fetched one round ahead;
-    // the LayerNorm statistics of its rows (one row per lane l < 32, shared by
-    // both rounds of j) are handed to the lanes that need them by lane
-    // permutes. The column vectors (bias, and for a LayerNorm residual its gain
-    // and offset, the offset folded into the bias) are read again each round
-    // (L1 hits) rather than held through the epilogue. Residual, statistics
+    // 128 x 128. The residual pieces of a round are fetched one round ahead,
+    // and the LayerNorm statistics of the lane's four rows (shared by both
+    // rounds of j) a j ahead, each lane loading its own rows' (a broadcast
+    // within the load: no lane permutes). The column vectors (bias, and for a
+    // LayerNorm residual its gain and offset, the offset folded into the bias;
+    // for a folded LayerNorm the weight's column sums) are read again each
+    // round (L1 hits) rather than held through the epilogue. Residual, statistics
     // and outputs go through raw buffer operations with 32-bit offsets: rows
     // past M lie beyond the resources, read as zeros and are not written.
     u32x4 rres[4];
-    LnRow stn{0.f, 0.f}, stc{0.f, 0.f};
+    LnRow stn[4], stc[4];  // statistics of the lane's rows er + 8 u (next j, current j)
     auto rload = [&](int j, int h) {
-      if (EPI >= EPI_BIAS_RESID) {
+      if (epi_resid(EPI)) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const uint32_t o = 2u * ((uint32_t)(cm0 + j * 32 + 8 * u) * (uint32_t)ldr + (uint32_t)(cn0 + 64 * h)) + lr;
           rres[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rr, (int)o, 0, 0));
         }
-        if (EPI == EPI_BIAS_RESLN && h == 0) {
-          const uint32_t o = 8u * (uint32_t)(cm0 + j * 32) + ls;
+      }
+      if (kStats && h == 0) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const uint32_t o = 8u * (uint32_t)(cm0 + j * 32 + 8 * u) + ls;
           const u32x2 v = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rs, (int)o, 0, 0));
-          stn = LnRow{__uint_as_float(v[0]), __uint_as_float(v[1])};
+          stn[u] = LnRow{__uint_as_float(v[0]), __uint_as_float(v[1])};
         }
       }
     };
@@ -473,7 +501,9 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
         u32x4 rcur[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) rcur[u] = rres[u];
-        if (h == 0) stc = stn;
+        if (h == 0)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) stc[u] = stn[u];
         if (j * 2 + h + 1 < 8) rload((j * 2 + h + 1) >> 1, (j * 2 + h + 1) & 1);
         asm volatile("" ::: "memory");  // keeps the column vectors from being held across rounds
         const int ncol = cn0 + wn * 128 + 64 * h + ec * 8;
@@ -481,10 +511,8 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
           cb[q] = *reinterpret_cast<const floatx4*>(bias + ncol + 4 * q);
-          if (EPI == EPI_BIAS_RESLN) {
-            cb[q] += *reinterpret_cast<const floatx4*>(ln.b + ncol + 4 * q);
-            lg[q] = *reinterpret_cast<const floatx4*>(ln.g + ncol + 4 * q);
-          }
+          if (EPI == EPI_BIAS_RESLN) cb[q] += *reinterpret_cast<const floatx4*>(ln.b + ncol + 4 * q);
+          if (kStats) lg[q] = *reinterpret_cast<const floatx4*>(ln.g + ncol + 4 * q);
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -493,9 +521,25 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
           const floatx4 x1 = *reinterpret_cast<const floatx4*>(park + r * 64 + (((2 * ec + 1) ^ (r & 15)) << 2));
           const uint32_t o_off = 2u * ((uint32_t)(cm0 + j * 32 + 8 * u) * (uint32_t)ldc + (uint32_t)(cn0 + 64 * h)) + lc;
           u32x4 ov;
-          if (EPI >= EPI_BIAS_RESID) {
+          if (epi_lnfold(EPI)) {
+            // LN(A) W + b = (acc * x + y * cs) + b' for the row's statistics (x, y)
+            const LnRow st = stc[u];
+            bf16x8 o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              float v0 = fmaf(x0[e], st.x, fmaf(st.y, lg[0][e], cb[0][e]));
+              float v1 = fmaf(x1[e], st.x, fmaf(st.y, lg[1][e], cb[1][e]));
+              if (epi_gelu(EPI)) {
+                v0 = gelu_erf(v0);
+                v1 = gelu_erf(v1);
+              }
+              o[e] = (bf16)v0;
+              o[e + 4] = (bf16)v1;
+            }
+            ov = __builtin_bit_cast(u32x4, o);
+          } else if (epi_resid(EPI)) {
             LnRow st{0.f, 0.f};
-            if (EPI == EPI_BIAS_RESLN) st = LnRow{__shfl(stc.x, r), __shfl(stc.y, r)};
+            if (EPI == EPI_BIAS_RESLN) st = stc[u];
             f16x8 o;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -534,7 +578,7 @@ __global__ __launch_bounds__(256) void gemm_plain(const T* __restrict__ A, int l
                                                   void* __restrict__ C, int ldc, int M, int N, int K, LnResid ln) {
   typedef SumT<T> S;
   typedef typename std::conditional<EPI == EPI_BIAS_RESLN, S, T>::type RT;  // residual element type
-  typedef typename std::conditional<(EPI >= EPI_BIAS_RESID), S, T>::type CT;  // output element type
+  typedef typename std::conditional<epi_resid(EPI), S, T>::type CT;  // output element type
   __shared__ float sA[16][64 + 4];
   __shared__ float sB[16][64 + 4];
   const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
@@ -599,21 +643,32 @@ static hipError_t plain(const void* A, int lda, const void* Bt, const float* bia
     case EPI_BIAS_GELU: TX_PL(EPI_BIAS_GELU); break;
     case EPI_BIAS_RESID: TX_PL(EPI_BIAS_RESID); break;
     case EPI_BIAS_RESLN: TX_PL(EPI_BIAS_RESLN); break;
+    default: return hipErrorInvalidValue;  // the LayerNorm-folding epilogues run on the persistent kernel only
   }
 #undef TX_PL
   return hipGetLastError();
 }
 
+// Shapes the persistent kernel takes without splitting rows: N a multiple of
+// the tile, K of two k steps and at least four, M at least 2048 rows (below,
+// the launch covers too few of the CUs), element offsets within int32.
+static bool persistent_shape(int M, int N, int K, long long ld_max) {
+  return N % PT == 0 && K % (2 * PK) == 0 && K >= 4 * PK && M >= 2048 && (long long)M * ld_max < (1ll << 31) &&
+         (long long)N * K < (1ll << 31);
+}
+bool gemm_ln_ok(int N, int K, int lda, int ldc) { return N % GN == 0 && K % GK == 0 && lda % 8 == 0 && ldc % 8 == 0; }
+
 hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const float* bias, const void* R, int ldr,
                        void* C, int ldc, int M, int N, int K, Epilogue epi, hipStream_t s, LnResid ln) {
   if (M <= 0) return hipSuccess;
   if (epi == EPI_BIAS_RESLN && (!ln.stats || !ln.g || !ln.b)) return hipErrorInvalidValue;
-  if (epi >= EPI_BIAS_RESID && !R) return hipErrorInvalidValue;
+  if (epi_resid(epi) && !R) return hipErrorInvalidValue;
+  if (epi_lnfold(epi) && (!bf || !ln.stats || !ln.g || !gemm_ln_ok(N, K, lda, ldc))) return hipErrorInvalidValue;
   if (!bf) return plain<float>(A, lda, Bt, bias, R, ldr, C, ldc, M, N, K, epi, ln, s);
   // The MFMA kernels address A, R and C with 32-bit byte offsets: a product
   // whose operands span 2^31 elements or more runs as several row chunks.
   {
-    const long long ld_max = std::max({(long long)lda, (long long)ldc, epi >= EPI_BIAS_RESID ? (long long)ldr : 1ll});
+    const long long ld_max = std::max({(long long)lda, (long long)ldc, epi_resid(epi) ? (long long)ldr : 1ll});
     const long long rows_max = std::max(256ll, ((1ll << 31) - 1) / ld_max / 256 * 256);
     if (M > rows_max) {
       for (long long m0 = 0; m0 < M; m0 += rows_max) {
@@ -638,8 +693,7 @@ hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const fl
   const bf16* b = (const bf16*)Bt;
   // Persistent kernel: K a multiple of 128 and at least 256 (its load stream
   // runs three k steps ahead), element offsets within int32.
-  if (N % PT == 0 && K % (2 * PK) == 0 && K >= 4 * PK && M >= 2048 && (long long)M * lda < (1ll << 31) &&
-      (long long)M * ldc < (1ll << 31) && (long long)M * ldr < (1ll << 31) && (long long)N * K < (1ll << 31)) {
+  if (persistent_shape(M, N, K, std::max({(long long)lda, (long long)ldc, (long long)ldr}))) {
     // the current device's CU count, looked up once per device
     static std::atomic<int> cu_of_device[64];
     int dev = 0, n_cu = 0;
@@ -662,6 +716,8 @@ hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const fl
       case EPI_BIAS_GELU: TX_GP4(EPI_BIAS_GELU); break;
       case EPI_BIAS_RESID: TX_GP4(EPI_BIAS_RESID); break;
       case EPI_BIAS_RESLN: TX_GP4(EPI_BIAS_RESLN); break;
+      case EPI_LN: TX_GP4(EPI_LN); break;
+      case EPI_LN_GELU: TX_GP4(EPI_LN_GELU); break;
     }
 #undef TX_GP4
     return hipGetLastError();
@@ -675,6 +731,8 @@ hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const fl
     case EPI_BIAS_GELU: TX_G128(EPI_BIAS_GELU); break;
     case EPI_BIAS_RESID: TX_G128(EPI_BIAS_RESID); break;
     case EPI_BIAS_RESLN: TX_G128(EPI_BIAS_RESLN); break;
+    case EPI_LN: TX_G128(EPI_LN); break;
+    case EPI_LN_GELU: TX_G128(EPI_LN_GELU); break;
   }
 #undef TX_G128
   return hipGetLastError();

@@ -105,9 +105,11 @@ __global__ __launch_bounds__(256) void layernorm_rows(const TX* __restrict__ x, 
       for (int e = 0; e < EPL; ++e) z[e] = fmaf(fmaf(v[e], inv, sh), gv[e], bv[e]);
       head_out<EPL>(z, c0, 1, EPL, lane, d, w, b0, scores, row, n_act);
     } else {
-      T* yr = y + (size_t)row * d + c0;
+      if (y) {
+        T* yr = y + (size_t)row * d + c0;
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) yr[e] = (T)fmaf(fmaf(v[e], inv, sh), gv[e], bv[e]);
+        for (int e = 0; e < EPL; ++e) yr[e] = (T)fmaf(fmaf(v[e], inv, sh), gv[e], bv[e]);
+      }
       if (stats && lane == 0) stats[row] = LnRow{inv, sh};
     }
   }
@@ -136,7 +138,8 @@ __global__ __launch_bounds__(256) void layernorm_rows_any(const TX* __restrict__
   const float inv = rsqrtf(sq / d + eps);
   const float sh = -mean * inv;
   if (!SCORE) {
-    for (int c = lane; c < d; c += 64) y[(size_t)row * d + c] = (T)fmaf(fmaf((float)xr[c], inv, sh), g[c], b[c]);
+    if (y)
+      for (int c = lane; c < d; c += 64) y[(size_t)row * d + c] = (T)fmaf(fmaf((float)xr[c], inv, sh), g[c], b[c]);
     if (stats && lane == 0) stats[row] = LnRow{inv, sh};
     return;
   }
@@ -345,6 +348,60 @@ hipError_t launch_to_f32(bool bf, const void* src, float* dst, int64_t n, hipStr
   const unsigned blocks = (unsigned)((n + 255) / 256);
   if (bf) to_f32_kernel<bf16><<<blocks, 256, 0, s>>>((const bf16*)src, dst, n);
   else to_f32_kernel<float><<<blocks, 256, 0, s>>>((const float*)src, dst, n);
+  return hipGetLastError();
+}
+
+// The LayerNorm fold of a consumer GEMM (EPI_LN*): for output column n of the
+// repacked weight Bt [N][K] (bf16), W'[n][k] = g[k] Bt[n][k] in fp16,
+// cs[n] = sum_k W'[n][k] (of the rounded values, as the GEMM multiplies them)
+// and b'[n] = bias[n] + sum_k lnb[k] Bt[n][k]. One block per column; the sums
+// run in a fixed order. *overflow is set when a scaled weight leaves the fp16
+// range (the caller then keeps the unfolded LayerNorm).
+__global__ __launch_bounds__(256) void fold_ln_weight(const bf16* __restrict__ Bt, int K, const float* __restrict__ g,
+                                                      const float* __restrict__ lnb, const float* __restrict__ bias,
+                                                      f16* __restrict__ Wf, float* __restrict__ cs,
+                                                      float* __restrict__ bf, int* __restrict__ overflow) {
+  __shared__ float part[2][4];
+  const int n = blockIdx.x, tid = threadIdx.x;
+  float c = 0.f, bb = 0.f;
+  bool bad = false;
+  for (int k = tid; k < K; k += 256) {
+    const float w = (float)Bt[(size_t)n * K + k];
+    const float gw = g[k] * w;
+    bad |= !(fabsf(gw) <= 65504.f);
+    const f16 wf = (f16)gw;
+    Wf[(size_t)n * K + k] = wf;
+    c += (float)wf;
+    bb = fmaf(lnb[k], w, bb);
+  }
+  if (bad) *overflow = 1;
+  c = wave_sum(c);
+  bb = wave_sum(bb);
+  if ((tid & 63) == 0) {
+    part[0][tid >> 6] = c;
+    part[1][tid >> 6] = bb;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    cs[n] = (part[0][0] + part[0][1]) + (part[0][2] + part[0][3]);
+    bf[n] = bias[n] + ((part[1][0] + part[1][1]) + (part[1][2] + part[1][3]));
+  }
+}
+
+__global__ void zero_int(int* p) { *p = 0; }
+hipError_t launch_zero_int(int* p, hipStream_t s) {
+  zero_int<<<1, 1, 0, s>>>(p);
+  return hipGetLastError();
+}
+hipError_t read_int(const int* dev, int* host, hipStream_t s) {
+  hipError_t e = hipMemcpyAsync(host, dev, sizeof(int), hipMemcpyDeviceToHost, s);
+  return e == hipSuccess ? hipStreamSynchronize(s) : e;
+}
+
+hipError_t launch_fold_ln_weight(const void* Bt, int N, int K, const float* g, const float* lnb, const float* bias,
+                                 void* Wf, float* cs, float* bf, int* overflow, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  fold_ln_weight<<<N, 256, 0, s>>>((const bf16*)Bt, K, g, lnb, bias, (f16*)Wf, cs, bf, overflow);
   return hipGetLastError();
 }
 

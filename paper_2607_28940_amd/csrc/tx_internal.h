@@ -127,9 +127,20 @@ struct PageGeom {
 //                   LN(R)[m][n] = (R[m][n] * st[m].x + st[m].y) * g[n] + b[n]
 //                   recomputes in fp32 the LayerNorm output whose rounded copy
 //                   the sublayer read as its operand       (C in the sum type)
+//   EPI_LN          C = LN(A) * W + b, computed as (acc * st[m].x + st[m].y *
+//   EPI_LN_GELU     cs[n]) + b'[n] (then GELU): the consumer of a LayerNorm
+//                   output multiplies the stored pre-LN sum itself (A in the
+//                   sum type, fp16) by the gain-scaled weight W'[k][n] =
+//                   g[k] W[k][n] (Bt in fp16), cs[n] = sum_k W'[k][n] and
+//                   b'[n] = b[n] + sum_k LNb[k] W[k][n] (ln.g = cs, bias = b');
+//                   bf16 models, MFMA-kernel shapes only (gemm_ln_ok)
+//                                                           (C in the model type)
 // The sum type holds a post-LN sublayer's pre-LayerNorm sum: fp16 for bf16
 // models (same width, 8x finer rounding), fp32 for fp32 models.
-enum Epilogue { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2, EPI_BIAS_RESLN = 3 };
+enum Epilogue { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2, EPI_BIAS_RESLN = 3, EPI_LN = 4, EPI_LN_GELU = 5 };
+__host__ __device__ constexpr bool epi_resid(int e) { return e == EPI_BIAS_RESID || e == EPI_BIAS_RESLN; }
+__host__ __device__ constexpr bool epi_gelu(int e) { return e == EPI_BIAS_GELU || e == EPI_LN_GELU; }
+__host__ __device__ constexpr bool epi_lnfold(int e) { return e == EPI_LN || e == EPI_LN_GELU; }
 
 // Row statistics of a LayerNorm in the form its consumers apply it:
 // x = 1 / sqrt(var + eps), y = -mean * x (so LN(v) = (v * x + y) * g + b).
@@ -144,11 +155,13 @@ struct LnResid {
 
 // C[M][N] (ldc) = epi(A[M][K] (lda) * Bt[N][K]^T + bias[N] (+ residual)).
 // C must not overlap A or R.
+bool gemm_ln_ok(int N, int K, int lda, int ldc);  // EPI_LN* runs on this shape (any M)
 hipError_t launch_gemm(bool bf, const void* A, int lda, const void* Bt, const float* bias, const void* R, int ldr,
                        void* C, int ldc, int M, int N, int K, Epilogue epi, hipStream_t s, LnResid ln = LnResid());
 
 // y[i] = LN(x[i]) * g + b over d features for M rows; x in the sum type, y in
-// the model type; the row statistics go to stats[i] when it is not null.
+// the model type; the row statistics go to stats[i] when it is not null. With
+// y null only the statistics are written (their consumers fold the LayerNorm).
 hipError_t launch_layernorm(bool bf, const void* x, void* y, LnRow* stats, const float* g, const float* b, int M,
                             int d, float eps, hipStream_t s);
 // Decoder head on LN(x[i]) = z_i, x in the sum type (fp32 out): n_act == 0: scores[i] = z_i . w + b0;
@@ -237,6 +250,16 @@ hipError_t static_scratch(void** out);
 
 // dst[n][k] = src[k][n] (src [K][N] row-major), same element type
 hipError_t launch_transpose(bool bf, const void* src, void* dst, int K, int N, int dst_ld, hipStream_t s);
+// The weight of a LayerNorm-folding GEMM (EPI_LN*) from the repacked bf16
+// weight Bt [N][K], the LayerNorm's gain g and offset lnb [K] and the bias [N]:
+// Wf [N][K] fp16 = g[k] Bt[n][k], cs[n] = sum_k Wf[n][k], bf[n] = bias[n] +
+// sum_k lnb[k] Bt[n][k]; *overflow set to 1 when a scaled weight is not finite
+// in fp16.
+hipError_t launch_fold_ln_weight(const void* Bt, int N, int K, const float* g, const float* lnb, const float* bias,
+                                 void* Wf, float* cs, float* bf, int* overflow, hipStream_t s);
+// *p = 0 on the stream; *host = *dev after the stream's work so far.
+hipError_t launch_zero_int(int* p, hipStream_t s);
+hipError_t read_int(const int* dev, int* host, hipStream_t s);
 // dst fp32 [N][K] = src [K][N]
 hipError_t launch_transpose_to_f32(bool bf, const void* src, float* dst, int K, int N, hipStream_t s);
 // dst fp32[n] = src[n]

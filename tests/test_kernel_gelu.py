@@ -2,13 +2,13 @@
 
 The FFN's activation is the exact erf GELU, x Phi(x) (Sec. 4.1.2). The HIP
 epilogue evaluates Phi(-|x|) = erfc(|x| / sqrt 2) / 2 in the form of Press et
-al. (erfc(z) = t exp(-z^2 + P(t)), t = 1 / (1 + z / 2)) with P a degree-7 fit
+al. (erfc(z) = t exp(-z^2 + P(t)), t = 1 / (1 + z / 2)) with P a degree-5 fit
 made by csrc/gelu_fit.py, the change to base 2 and the halving folded into
 its coefficients. This test reads the constants out of `gelu_erf` in the
 kernel source, checks that they are the fit script's, evaluates the formula
 in fp64 and compares it with scipy's erfc: a mistyped or wrongly rescaled
 coefficient, or a wrong sign in the final combination, shows up as an error
-far above the fit's 7.4e-7. (The kernel's fp32 constants and arithmetic add
+far above the fit's 8.2e-6. (The kernel's fp32 constants and arithmetic add
 rounding of order 1e-6, up to ~1e-5 in the far negative tail |x| > 8 where
 the squared exponent is large; the bf16 output resolves 4e-3.)
 """
@@ -21,7 +21,7 @@ from scipy.special import erfc
 
 CSRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2607_28940_amd", "csrc")
 SRC = os.path.join(CSRC, "gemm.hip")
-BOUND = 1e-6
+BOUND = 1e-5
 
 
 def _constants():
@@ -33,10 +33,10 @@ def _constants():
 
 def _formula(x):
     c = _constants()
-    # order in the source: t scale, 1.0, eight polynomial coefficients from
+    # order in the source: t scale, 1.0, six polynomial coefficients from
     # the highest power down, the scale of the exponent's square
-    assert len(c) == 11, c
-    t_scale, one, poly, w_scale = c[0], c[1], c[2:10], c[10]
+    assert len(c) == 9, c
+    t_scale, one, poly, w_scale = c[0], c[1], c[2:8], c[8]
     assert one == 1.0
     u = np.abs(x)
     t = 1.0 / (u * t_scale + one)
