@@ -773,17 +773,21 @@ __global__ __launch_bounds__(256, 2) void self_attn_mfma(const bf16* __restrict_
   }
   // a candidate's own key and value, fetched now so that their latency
   // overlaps the serving keys
+  // (V in 16-byte pieces: lane hi takes the 8-feature group 2 p + hi of each
+  // 16 features, and the halves the other lane of the query needs are
+  // exchanged just before use, so each load covers 32 contiguous bytes of the
+  // row instead of 16)
   bf16x8 kown[DH / 16];
-  bf16x4 vown[DH / 32][4];
+  u32x4_t vraw[DH / 32][2] = {};
   if (is_cand) {
     const bf16* kr = qkv + (size_t)row * ld + d + h * DH + 8 * hi;
 #pragma unroll
     for (int kk = 0; kk < DH / 16; ++kk) kown[kk] = *reinterpret_cast<const bf16x8*>(kr + 16 * kk);
-    const bf16* vr = qkv + (size_t)row * ld + 2 * d + h * DH + 4 * hi;
+    const bf16* vr = qkv + (size_t)row * ld + 2 * d + h * DH + 8 * hi;
 #pragma unroll
     for (int db = 0; db < DH / 32; ++db)
 #pragma unroll
-      for (int gq = 0; gq < 4; ++gq) vown[db][gq] = *reinterpret_cast<const bf16x4*>(vr + 32 * db + 8 * gq);
+      for (int p = 0; p < 2; ++p) vraw[db][p] = *reinterpret_cast<const u32x4_t*>(vr + 32 * db + 16 * p);
   }
   MfmaAcc<DH> acc;
   acc.init();
@@ -841,6 +845,21 @@ __global__ __launch_bounds__(256, 2) void self_attn_mfma(const bf16* __restrict_
     const float pself = exp2f((dot - m_new) * scale_log2);
     acc.l = acc.l * alpha + pself;
     acc.m = m_new;
+    // features 32 db + 8 gq + 4 hi .. + 3 of the own value: after swapping the
+    // upper half of lane hi = 0's group with the lower half of lane hi = 1's,
+    // dwords 0-1 of piece p hold group 2 p and dwords 2-3 group 2 p + 1
+    bf16x4 vown[DH / 32][4];
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        u32x4_t w = vraw[db][p];
+        const auto s0 = __builtin_amdgcn_permlane32_swap(w[0], w[2], false, false);
+        const auto s1 = __builtin_amdgcn_permlane32_swap(w[1], w[3], false, false);
+        const u32x2_t lo = {s0[0], s1[0]}, up = {s0[1], s1[1]};
+        vown[db][2 * p] = __builtin_bit_cast(bf16x4, lo);
+        vown[db][2 * p + 1] = __builtin_bit_cast(bf16x4, up);
+      }
 #pragma unroll
     for (int db = 0; db < DH / 32; ++db)
 #pragma unroll
