@@ -287,7 +287,10 @@ int score_candidates_static(const tx_kv_cache* cache, int32_t n_req, const int32
  * of the calls above is bracketed by a HIP event pair recorded on the caller's
  * stream, and tagged with its kernel class and the algorithmic flops and bytes
  * of that launch (the work the method defines for it, not what the kernel
- * happens to move). tx_profile_enable clears earlier records. */
+ * happens to move). tx_profile_enable clears earlier records; enabling makes
+ * 2048 events up front (call it while the GPU is idle: creating events while
+ * kernels run stalled a running kernel by milliseconds when the runtime grew
+ * its signal pool), enough for 1024 launches between reads. */
 int tx_profile_enable(int32_t on);
 /* Restricts recording to the classes whose bit (1 << class index) is set in
  * class_mask, so that a timed region carries event pairs only around the
