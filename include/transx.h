@@ -154,25 +154,37 @@ size_t tx_kv_page_bytes(const tx_config* cfg);
  * and the global token's cross-attention K/V of every decoder layer. */
 size_t tx_kv_pool_bytes(const tx_config* cfg, int64_t n_pages, int32_t max_requests, int64_t max_tokens);
 
-/* Create a cache over a caller-owned device pool (256-byte aligned). Request
- * ids are 0 .. max_requests-1. Also reserves the pinned host staging that
+/* Create a cache over a caller-owned device pool (256-byte aligned): the
+ * per-user store of encoded behavior K/V that amortized serving reads
+ * (Sec. 4.3; App. D, cache management, warm start: the caller builds entries
+ * ahead of serving). Request ids are 0 .. max_requests-1. Also reserves the pinned host staging that
  * score_candidates_static uploads its metadata through (4 x 512 KiB; without a
  * usable device the cache is still created and that call later reports
  * TX_E_NOMEM). Errors: TX_E_INVALID, TX_E_NOMEM (pool too small). */
 int tx_kv_cache_create(const tx_model* model, void* dev_pool, size_t pool_bytes, int64_t n_pages,
                        int32_t max_requests, int64_t max_tokens, tx_kv_cache** out);
+/* Release the cache's host bookkeeping (the caller frees the device pool
+ * afterwards, once the stream's work on it has completed). */
 void tx_kv_cache_destroy(tx_kv_cache* cache);
 
-/* Evict requests (their pages return to the free list). Releasing a request
- * without a cache is not an error. Errors: TX_E_INVALID (id out of range). */
+/* Evict requests (their pages return to the free list): the eviction step of
+ * the cache lifecycle (App. D, cache management: entries carry a time-to-live
+ * and are evicted by recency of access; the policy stays with the caller,
+ * this call frees the pages). Releasing a request without a cache is not an
+ * error. Errors: TX_E_INVALID (id out of range). */
 int tx_kv_cache_release(tx_kv_cache* cache, int32_t n_req, const int32_t* req_ids /* host */);
 
-/* Cached length of a request; -1 if it has no cache. */
+/* Cached length of a request (the encoded prefix that kv_cache_append
+ * extends, App. D nearline updates); -1 if it has no cache (cold start). */
 int tx_kv_cache_length(const tx_kv_cache* cache, int32_t req_id, int64_t* len_out /* host */);
 
+/* Pages on the free list: the headroom the caller's eviction policy (App. D
+ * cache lifecycle) works against. */
 int64_t tx_kv_cache_free_pages(const tx_kv_cache* cache);
 
-/* Model id the cache was created for (App. D cache versioning). */
+/* Model id the cache was created for (App. D, cache management, versioning
+ * and consistency: entries are tied to the model identifier, so a caller that
+ * upgrades the model creates a new cache instead of reusing stale entries). */
 uint64_t tx_kv_cache_model_id(const tx_kv_cache* cache);
 
 /* Copy one cached tensor of a request into a dense device buffer out
