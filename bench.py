@@ -326,8 +326,10 @@ def main():
     head = f"softmax over {m.n_actions} action tokens" if m.n_actions else "scalar logit head"
     append_info = None
     if args.append:
-        enc = {k: v for k, v in prof.items() if k.startswith("encode.")}
-        app_ms = sum(v["ms"] for v in enc.values()) / args.steps if enc else None
+        # the append's launches, from the untimed steps that bracket every
+        # launch (the timed steps bracket only the dominant class's)
+        enc = {k: v for k, v in prof_all.items() if k.startswith("encode.")}
+        app_ms = sum(v["ms"] for v in enc.values()) / args.profile_steps if enc else None
         append_info = {"events_per_step": wl.n_append * n_users,
                        "append_ms_per_step": round(app_ms, 4) if app_ms is not None else None,
                        "events_per_s": round(wl.n_append * n_users / (app_ms / 1e3), 1) if app_ms else None}
