@@ -67,7 +67,11 @@ CASES = [
     ("dh128-L64-pool", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16), 64, True, SHARP, BF16_TOL),
     ("dh64-L5-nopool", ModelConfig(256, 4, 512, 2, 1, rel_pos_buckets=0), 5, False, SHARP, BF16_TOL),
     # bf16 windows of at most 16 keys run on the dot2 kernel, longer ones on
-    # the general kernel: both sides of that boundary, and d_head 32
+    # the general kernel: both sides of that boundary, d_head 32, and windows
+    # of 12 and 13 keys with and without the pooled token
+    ("dh32-L12-pool", ModelConfig(64, 2, 256, 1, 2, rel_pos_buckets=8), 12, True, SHARP, BF16_TOL),
+    ("dh128-L13-nopool", ModelConfig(256, 2, 1024, 2, 1, rel_pos_buckets=0), 13, False, SHARP, BF16_TOL),
+    ("dh64-L13-pool", ModelConfig(256, 4, 512, 2, 2, rel_pos_buckets=16), 13, True, SHARP, BF16_TOL),
     ("dh32-L15-pool", ModelConfig(64, 2, 256, 1, 2, rel_pos_buckets=8), 15, True, SHARP, BF16_TOL),
     ("dh64-L16-nopool", ModelConfig(256, 4, 512, 2, 1, rel_pos_buckets=0), 16, False, SHARP, BF16_TOL),
     ("dh128-L16-pool", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16), 16, True, SHARP, BF16_TOL),
