@@ -1,16 +1,15 @@
 """The GEMM epilogue's GELU formula, checked on the CPU (no GPU needed).
 
 The FFN's activation is the exact erf GELU, x Phi(x) (Sec. 4.1.2). The HIP
-epilogue evaluates Phi(-|x|) = erfc(|x| / sqrt 2) / 2 in the form of Press et
-al. (erfc(z) = t exp(-z^2 + P(t)), t = 1 / (1 + z / 2)) with P a degree-5 fit
-made by csrc/gelu_fit.py, the change to base 2 and the halving folded into
-its coefficients. This test reads the constants out of `gelu_erf` in the
-kernel source, checks that they are the fit script's, evaluates the formula
-in fp64 and compares it with scipy's erfc: a mistyped or wrongly rescaled
-coefficient, or a wrong sign in the final combination, shows up as an error
-far above the fit's 8.2e-6. (The kernel's fp32 constants and arithmetic add
-rounding of order 1e-6, up to ~1e-5 in the far negative tail |x| > 8 where
-the squared exponent is large; the bf16 output resolves 4e-3.)
+epilogue evaluates it as max(x, 0) - |x| Phi(-|x|) with Phi(-u) = 2^Q(min(u, 6))
+and Q a degree-7 polynomial fitted to log2 Phi(-u) by csrc/gelu_fit.py. This
+test reads the constants out of `gelu_erf` in the kernel source, checks that
+they are the fit script's, evaluates the formula with the kernel's fp32
+arithmetic (Horner steps rounded to fp32) and compares it with scipy's erfc:
+a mistyped coefficient, a wrong clamp or a wrong sign in the final
+combination shows up as an error far above the fit's 5.5e-6. Beyond the
+clamp |GELU(x)| < |x| Phi(-6) < 1e-9 |x|, and that is the bound there (the
+bf16 output resolves 4e-3 of a value).
 """
 import importlib.util
 import os
@@ -21,7 +20,8 @@ from scipy.special import erfc
 
 CSRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2607_28940_amd", "csrc")
 SRC = os.path.join(CSRC, "gemm.hip")
-BOUND = 1e-5
+BOUND = 1e-5       # fractional error, |x| <= 6
+TAIL_BOUND = 1e-9  # absolute error over |x|, |x| > 6
 
 
 def _constants():
@@ -33,42 +33,43 @@ def _constants():
 
 def _formula(x):
     c = _constants()
-    # order in the source: t scale, 1.0, six polynomial coefficients from
-    # the highest power down, the scale of the exponent's square
+    # order in the source: the clamp, eight coefficients from the highest
+    # power down
     assert len(c) == 9, c
-    t_scale, one, poly, w_scale = c[0], c[1], c[2:8], c[8]
-    assert one == 1.0
-    u = np.abs(x)
-    t = 1.0 / (u * t_scale + one)
-    p = np.full_like(x, poly[0])
+    clamp, poly = np.float32(c[0]), [np.float32(v) for v in c[1:]]
+    xf = x.astype(np.float32)
+    u = np.minimum(np.abs(xf), clamp)
+    q = np.full_like(u, poly[0])
     for k in poly[1:]:
-        p = p * t + k
-    w = u * w_scale
-    q = t * np.exp2(p - w * w)
-    return np.maximum(x, 0.0) - u * q, q
+        q = (q * u + k).astype(np.float32)
+    phi = np.exp2(q.astype(np.float64))
+    return np.maximum(x, 0.0) - np.abs(x) * phi, phi
 
 
 def test_constants_are_the_fit():
     spec = importlib.util.spec_from_file_location("gelu_fit", os.path.join(CSRC, "gelu_fit.py"))
     mod = importlib.util.module_from_spec(spec)
     spec.loader.exec_module(mod)
-    coef, t_scale, w_scale = mod.fit()
+    coef, clamp = mod.fit()
     c = _constants()
-    want = [t_scale, 1.0] + list(coef) + [w_scale]
+    want = [clamp] + list(coef)
     assert np.allclose(c, want, rtol=1e-12, atol=0), (c, want)
 
 
-def test_phi_tail_relative_error():
-    x = np.linspace(-14.0, 14.0, 400001)
+def test_phi_relative_error():
+    x = np.linspace(-6.0, 6.0, 400001)
     _, q = _formula(x)
     phi = 0.5 * erfc(np.abs(x) / np.sqrt(2.0))  # Phi(-|x|)
     assert np.max(np.abs(q / phi - 1.0)) < BOUND
 
 
-def test_gelu_relative_error():
-    x = np.concatenate([np.linspace(-14.0, 14.0, 400001), [-1e-30, 1e-30, 0.0]])
+def test_gelu_error():
+    x = np.concatenate([np.linspace(-14.0, 14.0, 400001), [-1e-30, 1e-30, 0.0, -1e4, 1e4]])
     g, _ = _formula(x)
     ref = 0.5 * x * erfc(-x / np.sqrt(2.0))
-    nz = ref != 0
+    inner = np.abs(x) <= 6.0
+    nz = inner & (ref != 0)
     assert np.max(np.abs(g[nz] / ref[nz] - 1.0)) < BOUND
-    assert np.all(g[~nz] == 0.0)
+    assert np.all(g[inner & (ref == 0)] == 0.0)
+    out = ~inner
+    assert np.max(np.abs(g[out] - ref[out]) / np.abs(x[out])) < TAIL_BOUND
