@@ -332,16 +332,22 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_p4(const bf16* __restrict__ 
   };
   using F0 = std::false_type;
   using T1 = std::true_type;
-  // 16 MFMAs with 8 fragment reads, 4 LDS stores and 4 global loads between them
+  // 16 MFMAs with 8 fragment reads, 4 LDS stores and 4 global loads between
+  // them: the reads (the next sub-step's fragments) between the first eight
+  // MFMAs, so that they have the second half to land, then the stores and
+  // loads (~1% faster than spreading the reads over all sixteen)
   auto interleave = [&]() {
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
     }
