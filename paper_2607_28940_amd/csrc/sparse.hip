@@ -231,8 +231,15 @@ __global__ __launch_bounds__(256) void lg_cross_attn(const T* __restrict__ q, in
 // PV over the pairs, one dot2 per pair and feature, with the probabilities
 // rounded to bf16 (as the dense kernels round P) and l summed over the
 // rounded values.
+// A block serves every query of its (request, head), 128 at a time, so the
+// window is staged once per (request, head): a page's V^T slab holds one
+// 128-byte line per feature, and a window's values, 4 KB of them, touch 128
+// such lines per head (staged per 128 queries, those line reads took a fifth
+// of the launch). The next 128 queries' Q pieces are requested before the
+// current ones are worked on.
 constexpr int kLgDotKeys = 16;
-constexpr int kLgDotQueries = 128;  // queries per block (4 lanes each)
+constexpr int kLgDotQueries = 128;  // queries per pass of a block (4 lanes each)
+constexpr int kLgDotTile = 1 << 20;  // queries per tile: the whole request
 constexpr int kLgQueries = 64;      // queries per block of the general kernel
 constexpr int kLgDotPairs = kLgDotKeys / 2 + 2;  // window + alignment + pooled token
 
@@ -251,18 +258,23 @@ __global__ __launch_bounds__(4 * kLgDotQueries) void lg_cross_attn_dot(const bf1
   const AttnTile tile = tiles[blockIdx.x];
   if (tile.q_count <= 0) return;
   const AttnReq rq = reqs[tile.req];
-  const int h = tile.head, tid = threadIdx.x, qi = tid >> 2, part = tid & 3;
-  const bool active = qi < tile.q_count;
-  // the query's Q pieces, requested first
-  bf16x8 qv[NP];
-  int row = 0;
-  if (active) {
-    const int i = tile.q_begin + qi;
-    row = i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
+  const int h = tile.head, tid = threadIdx.x, part = tid & 3;
+  // the Q pieces of query q_begin + qc + tid / 4, when the tile has it
+  auto q_row = [&](int qc) {
+    const int i = tile.q_begin + qc + (tid >> 2);
+    return i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
+  };
+  auto load_q = [&](int qc, bf16x8(&qv)[NP]) {
+    if (qc + (tid >> 2) < tile.q_count) {
+      const int row = q_row(qc);
 #pragma unroll
-    for (int e = 0; e < NP; ++e)
-      qv[e] = *reinterpret_cast<const bf16x8*>(q + (size_t)row * ldq + h * DH + (e * 4 + part) * 8);
-  }
+      for (int e = 0; e < NP; ++e)
+        qv[e] = *reinterpret_cast<const bf16x8*>(q + (size_t)row * ldq + h * DH + (e * 4 + part) * 8);
+    }
+  };
+  // the first 128 queries' Q pieces, requested first
+  bf16x8 qv[NP], qn[NP];
+  load_q(0, qv);
   const int len = rq.kv_len;
   const int k0 = max(0, len - l_local);
   const int a0 = k0 >> 1, npl = ((len - 1) >> 1) - a0 + 1;  // local pairs
@@ -305,7 +317,6 @@ __global__ __launch_bounds__(4 * kLgDotQueries) void lg_cross_attn_dot(const bf1
     sV[a * DH + f] = w;
   }
   __syncthreads();
-  if (!active) return;
   // slot j is a key unless it lies outside the window (slot 0 below k0, the
   // window's last slot at len) or is the pooled token's zero partner
   auto is_key = [&](int j) {
@@ -313,70 +324,258 @@ __global__ __launch_bounds__(4 * kLgDotQueries) void lg_cross_attn_dot(const bf1
     if (j < 2 * npl) return p0 + j >= k0 && p0 + j < len;
     return j == 2 * npl;
   };
-  float s[MS];
-  float m = -INFINITY;
+  for (int qc = 0; qc < tile.q_count; qc += kLgDotQueries) {
+    if (qc + kLgDotQueries < tile.q_count) load_q(qc + kLgDotQueries, qn);
+    if (qc + (tid >> 2) < tile.q_count) {
+      float s[MS];
+      float m = -INFINITY;
 #pragma unroll
-  for (int j = 0; j < MS; ++j) {
-    s[j] = -INFINITY;
-    if (is_key(j)) {
-      float acc = 0.f;
+      for (int j = 0; j < MS; ++j) {
+        s[j] = -INFINITY;
+        if (is_key(j)) {
+          float acc = 0.f;
 #pragma unroll
-      for (int e = 0; e < NP; ++e) {
-        const bf16x8 k8 = *reinterpret_cast<const bf16x8*>(sK + j * DH + (e * 4 + part) * 8);
+          for (int e = 0; e < NP; ++e) {
+            const bf16x8 k8 = *reinterpret_cast<const bf16x8*>(sK + j * DH + (e * 4 + part) * 8);
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-          acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{qv[e][2 * c], qv[e][2 * c + 1]},
-                                                bf16x2{k8[2 * c], k8[2 * c + 1]}, acc, false);
-      }
-      s[j] = quad_sum(acc) * scale_log2;
-      m = fmaxf(m, s[j]);
-    }
-  }
-  bf16 pb[MS];
-  float l = 0.f;
-#pragma unroll
-  for (int j = 0; j < MS; ++j) {
-    pb[j] = (bf16)__builtin_amdgcn_exp2f(s[j] - m);  // 0 where masked
-    l += (float)pb[j];
-  }
-  float o[NP][8];
-#pragma unroll
-  for (int e = 0; e < NP; ++e)
-#pragma unroll
-    for (int c = 0; c < 8; ++c) o[e][c] = 0.f;
-#pragma unroll
-  for (int a = 0; a < MP; ++a) {
-    if (a < np) {
-      const bf16x2 pp = {pb[2 * a], pb[2 * a + 1]};
-#pragma unroll
-      for (int e = 0; e < NP; ++e) {
-        // features (e * 4 + part) * 8 .. + 7 of the pair, 16 bytes per 4 features
-        // (taken apart element-wise: this compiler folds a bit_cast of u32
-        // vector element c to element 0)
-        const bf16* vr = reinterpret_cast<const bf16*>(sV + a * DH + (e * 4 + part) * 8);
-        const bf16x8 v0 = *reinterpret_cast<const bf16x8*>(vr);
-        const bf16x8 v1 = *reinterpret_cast<const bf16x8*>(vr + 8);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          o[e][c] = __builtin_amdgcn_fdot2_f32_bf16(pp, bf16x2{v0[2 * c], v0[2 * c + 1]}, o[e][c], false);
-          o[e][4 + c] = __builtin_amdgcn_fdot2_f32_bf16(pp, bf16x2{v1[2 * c], v1[2 * c + 1]}, o[e][4 + c], false);
+            for (int c = 0; c < 4; ++c)
+              acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{qv[e][2 * c], qv[e][2 * c + 1]},
+                                                    bf16x2{k8[2 * c], k8[2 * c + 1]}, acc, false);
+          }
+          s[j] = quad_sum(acc) * scale_log2;
+          m = fmaxf(m, s[j]);
         }
       }
+      bf16 pb[MS];
+      float l = 0.f;
+#pragma unroll
+      for (int j = 0; j < MS; ++j) {
+        pb[j] = (bf16)__builtin_amdgcn_exp2f(s[j] - m);  // 0 where masked
+        l += (float)pb[j];
+      }
+      float o[NP][8];
+#pragma unroll
+      for (int e = 0; e < NP; ++e)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) o[e][c] = 0.f;
+#pragma unroll
+      for (int a = 0; a < MP; ++a) {
+        if (a < np) {
+          const bf16x2 pp = {pb[2 * a], pb[2 * a + 1]};
+#pragma unroll
+          for (int e = 0; e < NP; ++e) {
+            // features (e * 4 + part) * 8 .. + 7 of the pair, 16 bytes per 4
+            // features (taken apart element-wise: this compiler folds a
+            // bit_cast of u32 vector element c to element 0)
+            const bf16* vr = reinterpret_cast<const bf16*>(sV + a * DH + (e * 4 + part) * 8);
+            const bf16x8 v0 = *reinterpret_cast<const bf16x8*>(vr);
+            const bf16x8 v1 = *reinterpret_cast<const bf16x8*>(vr + 8);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+              o[e][c] = __builtin_amdgcn_fdot2_f32_bf16(pp, bf16x2{v0[2 * c], v0[2 * c + 1]}, o[e][c], false);
+              o[e][4 + c] = __builtin_amdgcn_fdot2_f32_bf16(pp, bf16x2{v1[2 * c], v1[2 * c + 1]}, o[e][4 + c], false);
+            }
+          }
+        }
+      }
+      const float inv = 1.f / l;
+      const int row = q_row(qc);
+#pragma unroll
+      for (int e = 0; e < NP; ++e) {
+        bf16x8 w;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) w[c] = (bf16)(o[e][c] * inv);
+        *reinterpret_cast<bf16x8*>(out + (size_t)row * ldo + h * DH + (e * 4 + part) * 8) = w;
+      }
     }
+#pragma unroll
+    for (int e = 0; e < NP; ++e) qv[e] = qn[e];
   }
-  const float inv = 1.f / l;
+}
+
+// The same windows on matrix cores, for windows that fit 16 key slots after
+// their start is rounded down to a multiple of 4 (l_local + 1 <= 13 with the
+// pooled token, the paper's 10 + 1 included). Every query of a
+// (request, head) sees the same keys, so per group of 16 queries the scores
+// are one small product S^T = K Q^T (v_mfma_f32_16x16x32_bf16, keys as rows:
+// lane (q, g) ends with slots 4 g .. 4 g + 3 of query q) and the output one
+// more, O^T = V^T P^T (v_mfma_f32_16x16x16_bf16), whose P^T operand wants
+// exactly that layout: four slots of one query per lane. The softmax runs in
+// the accumulator registers (row maximum and sum over the query's four lanes
+// by row swaps), and no value changes lanes between the two products.
+// Slot j is cache position p0 + j with p0 = k0 rounded down to a multiple of
+// 4, and the pooled token takes the slot of position len; four slots are
+// four consecutive positions, which a page's V^T slab keeps side by side (its
+// column permutation moves bits 2 and 3 of the position only), so V^T is
+// staged in 8-byte quads and K in 16-byte row pieces. Slots outside the
+// window are masked and staged as zeros (nothing past the request's cached
+// positions is read), so stale or poisoned page contents cannot reach the
+// result. A block of 4 waves serves every query of its (request, head), wave
+// w taking the groups of 16 queries w, w + 4, ..., the next group's Q
+// fragments requested before the current one is worked on. The output
+// accumulator holds 4 features of one query per lane and 16-feature chunk;
+// two row swaps per pair of chunks leave each lane 8 consecutive features,
+// so every 16-byte store covers 64 contiguous bytes of a row per query, as do
+// the Q loads (the B operand: 8 consecutive features per lane).
+constexpr int kLgMfmaSlots = 16;
+
+template <int DH>
+__global__ __launch_bounds__(256) void lg_cross_attn_mfma(const bf16* __restrict__ q, int ldq, bf16* __restrict__ out,
+                                                          int ldo, const bf16* __restrict__ pool,
+                                                          const int32_t* __restrict__ page_table, int max_pages,
+                                                          PageGeom g, int layer_slot, const AttnReq* __restrict__ reqs,
+                                                          const AttnTile* __restrict__ tiles, int l_local,
+                                                          const bf16* __restrict__ gkv, int gkv_ld, int dec_layer,
+                                                          float scale_log2) {
+  constexpr int NC = DH / 32;       // k chunks of the score product
+  constexpr int NO = DH / 16;       // feature chunks of the output product
+  constexpr int NS = kLgMfmaSlots;
+  constexpr int KS = DH + 8;        // K row stride (elements): rows 16 bytes apart in the banks
+  constexpr int VS = NS + 4;        // V^T row stride (elements)
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  __shared__ __attribute__((aligned(16))) bf16 sK[NS * KS];
+  __shared__ __attribute__((aligned(16))) bf16 sV[DH * VS];
+  const AttnTile tile = tiles[blockIdx.x];
+  if (tile.q_count <= 0) return;
+  const AttnReq rq = reqs[tile.req];
+  const int h = tile.head, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int qn = lane & 15, kg = lane >> 4;
+  const int n_groups = (tile.q_count + 15) / 16;
+  // Q fragments of group gi (features 32 c + 8 kg .. of query qn; zeros past
+  // the tile), and the query's output row
+  auto q_row = [&](int gi) {
+    const int i = tile.q_begin + 16 * gi + qn;
+    return i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
+  };
+  auto load_q = [&](int gi, bf16x8(&qf)[NC]) {
+    const bool ok = gi < n_groups && 16 * gi + qn < tile.q_count;
+    const int row = ok ? q_row(gi) : 0;
 #pragma unroll
-  for (int e = 0; e < NP; ++e) {
-    bf16x8 w;
+    for (int c = 0; c < NC; ++c)
+      qf[c] = ok ? *reinterpret_cast<const bf16x8*>(q + (size_t)row * ldq + h * DH + 32 * c + 8 * kg) : bf16x8{};
+  };
+  bf16x8 qa[NC], qb[NC];
+  load_q(wave, qa);
+  const int len = rq.kv_len;
+  const int k0 = max(0, len - l_local), p0 = k0 & ~3;
+  const bool gpool = gkv != nullptr;
+  auto is_key = [&](int p) { return (p >= k0 && p < len) || (gpool && p == len); };
+  // the window's (at most two) pages: the slots' cached positions end at len - 1
+  const int32_t* ptab = page_table + (size_t)rq.slot * max_pages;
+  const int pg0 = p0 / kPage, pg1 = max(pg0, (len - 1) / kPage);
+  const bf16* page0 = pool + (size_t)ptab[pg0] * g.page_elems;
+  const bf16* page1 = pool + (size_t)ptab[pg1] * g.page_elems;
+  auto page_of = [&](int p) { return p / kPage == pg0 ? page0 : page1; };
+  const int d = g.H * DH;
+  const bf16* grow = gpool ? gkv + (size_t)rq.slot * gkv_ld + (size_t)(2 * dec_layer) * d + h * DH : nullptr;
+  // K pieces (slot e / (DH / 8), features 8 (e % (DH / 8)) ..) and V^T quads
+  // (feature e / 4, slots 4 (e % 4) ..), zeros outside the window
+  for (int e = tid; e < NS * DH / 8; e += 256) {
+    const int j = e / (DH / 8), c = e % (DH / 8), p = p0 + j;
+    bf16x8 v = {};
+    if (p >= k0 && p < len)
+      v = *reinterpret_cast<const bf16x8*>(page_of(p) + g.k_off(layer_slot, h) + (size_t)(p % kPage) * DH + 8 * c);
+    else if (gpool && p == len)
+      v = *reinterpret_cast<const bf16x8*>(grow + 8 * c);
+    *reinterpret_cast<bf16x8*>(sK + j * KS + 8 * c) = v;
+  }
+  for (int e = tid; e < DH * NS / 4; e += 256) {
+    const int f = e / 4, pq = p0 + 4 * (e % 4);
+    bf16x4 v = {};
+    if (pq < len)
+      v = *reinterpret_cast<const bf16x4*>(page_of(pq) + g.v_off(layer_slot, h) + (size_t)f * kPage + vt_col(pq % kPage));
 #pragma unroll
-    for (int c = 0; c < 8; ++c) w[c] = (bf16)(o[e][c] * inv);
-    *reinterpret_cast<bf16x8*>(out + (size_t)row * ldo + h * DH + (e * 4 + part) * 8) = w;
+    for (int r = 0; r < 4; ++r) {
+      if (pq + r >= len) v[r] = (bf16)0.f;
+      if (gpool && pq + r == len) v[r] = grow[d + f];
+    }
+    *reinterpret_cast<bf16x4*>(sV + f * VS + 4 * (e % 4)) = v;
+  }
+  __syncthreads();
+  // A operands, read from LDS per group (holding them would cost the
+  // registers of two more resident waves per SIMD): K (slot qn, features
+  // 32 c + 8 kg ..) and V^T (feature 16 c + qn, slots 4 kg ..)
+  // (the lane offsets pass through an empty asm per group, so the reads are
+  // not hoisted out of the group loop)
+  const int kofs = qn * KS + 8 * kg, vofs = qn * VS + 4 * kg;
+  int ko = kofs, vo = vofs;
+  auto kfrag = [&](int c) { return *reinterpret_cast<const bf16x8*>(sK + ko + 32 * c); };
+  auto vfrag = [&](int c) { return *reinterpret_cast<const s16x4*>(sV + vo + 16 * VS * c); };
+  bool key[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) key[r] = is_key(p0 + 4 * kg + r);
+  auto group = [&](int gi, const bf16x8(&qf)[NC]) {
+    ko = kofs;
+    vo = vofs;
+    asm volatile("" : "+v"(ko), "+v"(vo));
+    floatx4 sc = {};
+#pragma unroll
+    for (int c = 0; c < NC; ++c) sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kfrag(c), qf[c], sc, 0, 0, 0);
+    // sc[r]: slot 4 kg + r of query qn
+    float m = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      sc[r] = key[r] ? sc[r] * scale_log2 : -INFINITY;
+      m = fmaxf(m, sc[r]);
+    }
+    m = xor32_max(row16_max(m));
+    bf16x4 pb;
+    float l = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      pb[r] = (bf16)__builtin_amdgcn_exp2f(sc[r] - m);  // 0 where masked
+      l += (float)pb[r];
+    }
+    l = xor32_sum(row16_sum(l));
+    const float inv = 1.f / l;
+    const s16x4 pp = __builtin_bit_cast(s16x4, pb);
+    const bool ok = 16 * gi + qn < tile.q_count;
+    const int row = ok ? q_row(gi) : 0;
+#pragma unroll
+    for (int c = 0; c < NO; c += 2) {
+      // o0[r], o1[r]: features 16 c + 4 kg + r and 16 (c + 1) + 4 kg + r
+      const floatx4 o0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vfrag(c), pp, floatx4{}, 0, 0, 0);
+      const floatx4 o1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vfrag(c + 1), pp, floatx4{}, 0, 0, 0);
+      bf16x4 b0, b1;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        b0[r] = (bf16)(o0[r] * inv);
+        b1[r] = (bf16)(o1[r] * inv);
+      }
+      u32x2_t x = __builtin_bit_cast(u32x2_t, b0), y = __builtin_bit_cast(u32x2_t, b1);
+      // lanes of key groups 2, 3 trade x for the y of groups 0, 1, then odd
+      // groups trade x for the y of even ones: group kg ends with features
+      // 16 c + 8 kg .. + 7 as (x, y)
+#pragma unroll
+      for (int w = 0; w < 2; ++w) {
+        const auto a = __builtin_amdgcn_permlane32_swap(x[w], y[w], false, false);
+        const auto b = __builtin_amdgcn_permlane16_swap(a[0], a[1], false, false);
+        x[w] = b[0];
+        y[w] = b[1];
+      }
+      if (ok) {
+        const u32x4_t unit = {x[0], x[1], y[0], y[1]};
+        *reinterpret_cast<u32x4_t*>(out + (size_t)row * ldo + h * DH + 16 * c + 8 * kg) = unit;
+      }
+    }
+  };
+  // groups wave, wave + 4, ...: two at a time, alternating the Q registers
+  for (int gi = wave; gi < n_groups; gi += 8) {
+    load_q(gi + 4, qb);
+    group(gi, qa);
+    if (gi + 4 >= n_groups) break;
+    load_q(gi + 8, qa);
+    group(gi + 4, qb);
   }
 }
 
 static bool lg_dot_path(bool bf, int l_local, bool gpool) { return bf && l_local + (gpool ? 1 : 0) <= kLgDotKeys; }
+// the window, started at a multiple of 4, and the pooled token within 16 slots
+static bool lg_mfma_path(bool bf, int l_local, bool gpool) {
+  return bf && l_local + (gpool ? 1 : 0) + 3 <= kLgMfmaSlots;
+}
 int lg_attention_q_block(bool bf, int l_local, bool gpool) {
-  return lg_dot_path(bf, l_local, gpool) ? kLgDotQueries : kLgQueries;
+  return lg_dot_path(bf, l_local, gpool) ? kLgDotTile : kLgQueries;
 }
 
 hipError_t launch_lg_attention(bool bf, const void* q, int ldq, void* out, int ldo, const void* pool,
@@ -387,6 +586,20 @@ hipError_t launch_lg_attention(bool bf, const void* q, int ldq, void* out, int l
   if (l_local < 1 || l_local > kMaxLocal) return hipErrorInvalidValue;
   if (q_block != lg_attention_q_block(bf, l_local, gkv != nullptr)) return hipErrorInvalidValue;
   const float sl2 = 1.4426950408889634f / sqrtf((float)g.dh);
+  if (lg_mfma_path(bf, l_local, gkv != nullptr)) {
+#define TX_LGM(DH)                                                                                          \
+  lg_cross_attn_mfma<DH><<<n_tiles, 256, 0, s>>>((const bf16*)q, ldq, (bf16*)out, ldo, (const bf16*)pool,          \
+                                                 page_table, max_pages, g, layer_slot, reqs, tiles, l_local,       \
+                                                 (const bf16*)gkv, gkv_ld, dec_layer, sl2)
+    switch (g.dh) {
+      case 32: TX_LGM(32); break;
+      case 64: TX_LGM(64); break;
+      case 128: TX_LGM(128); break;
+      default: return hipErrorInvalidValue;
+    }
+#undef TX_LGM
+    return hipGetLastError();
+  }
   if (lg_dot_path(bf, l_local, gkv != nullptr)) {
 #define TX_LGD(DH)                                                                                             \
   lg_cross_attn_dot<DH><<<n_tiles, 4 * kLgDotQueries, 0, s>>>((const bf16*)q, ldq, (bf16*)out, ldo, (const bf16*)pool,      \
