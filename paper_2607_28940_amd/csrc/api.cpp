@@ -1207,7 +1207,9 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
     mx = std::max<int64_t>(mx, S + C);
   }
   const bool sparse = m->l_local > 0;
-  const int qb = sparse ? lg_attention_q_block(bf, m->l_local, m->gpool) : paged_attention_q_block(bf, m->dh);
+  const int qb = sparse ? lg_attention_q_block(bf, m->l_local, m->gpool, H) : paged_attention_q_block(bf, m->dh);
+  // heads per tile group: one tile serves every head on the sparse MFMA kernel
+  const int th = sparse && lg_attention_all_heads(bf, m->l_local, m->gpool, H) ? 1 : H;
   const int sqb = self_attention_q_block(bf, m->dh);
   std::vector<AttnTile> t_full, t_cand;
   std::vector<SelfTile> s_full, s_cand;
@@ -1216,11 +1218,11 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
   XPlan x_full, x_cand;
   if (m->n_dec > 1) {
     if (xpipe) xattn_plan(full, H, xblocks, kXMaxParts, x_full);
-    else attn_tiles(full, H, qb, false, t_full);
+    else attn_tiles(full, th, qb, false, t_full);
     self_tiles(sreq, H, sqb, false, s_full);
   }
   if (xpipe) xattn_plan(cand, H, xblocks, kXMaxParts, x_cand);
-  else attn_tiles(cand, H, qb, false, t_cand);
+  else attn_tiles(cand, th, qb, false, t_cand);
   self_tiles(sreq, H, sqb, true, s_cand);
   Meta meta;
   const size_t o_sreq = meta.put(sreq), o_full = meta.put(full), o_cand = meta.put(cand);

@@ -410,17 +410,25 @@ __global__ __launch_bounds__(4 * kLgDotQueries) void lg_cross_attn_dot(const bf1
 // staged in 8-byte quads and K in 16-byte row pieces. Slots outside the
 // window are masked and staged as zeros (nothing past the request's cached
 // positions is read), so stale or poisoned page contents cannot reach the
-// result. A block of 4 waves serves every query of its (request, head), wave
-// w taking the groups of 16 queries w, w + 4, ..., the next group's Q
-// fragments requested before the current one is worked on. The output
-// accumulator holds 4 features of one query per lane and 16-feature chunk;
-// two row swaps per pair of chunks leave each lane 8 consecutive features,
-// so every 16-byte store covers 64 contiguous bytes of a row per query, as do
-// the Q loads (the B operand: 8 consecutive features per lane).
+// result.
+// A block serves up to kLgMfmaTile queries of one request for every head:
+// it stages the windows of all heads once, and its 8 waves take (group of
+// 16 queries, head) pairs eight consecutive ones at a time (with 8 heads, the
+// 8 head pieces of the same 16 rows), the next pair's Q fragments requested
+// before the current one is worked on. So each query's Q row is read, and
+// its O row written, as a whole 2 KB row within a short span (head by head
+// in blocks of their own, the 256-byte pieces of a row went to memory far
+// apart in time, and the launch ran at the ~4 TB/s such a sweep gets). The output accumulator holds 4
+// features of one query per lane and 16-feature chunk; two row swaps per
+// pair of chunks leave each lane 8 consecutive features, so every 16-byte
+// store covers 64 contiguous bytes of a row per query, as do the Q loads
+// (the B operand: 8 consecutive features per lane).
 constexpr int kLgMfmaSlots = 16;
+constexpr int kLgMfmaTile = 288;   // queries per tile
+constexpr int kLgMfmaHeads = 8;    // heads per block (the model's, at most)
 
 template <int DH>
-__global__ __launch_bounds__(256) void lg_cross_attn_mfma(const bf16* __restrict__ q, int ldq, bf16* __restrict__ out,
+__global__ __launch_bounds__(512) void lg_cross_attn_mfma(const bf16* __restrict__ q, int ldq, bf16* __restrict__ out,
                                                           int ldo, const bf16* __restrict__ pool,
                                                           const int32_t* __restrict__ page_table, int max_pages,
                                                           PageGeom g, int layer_slot, const AttnReq* __restrict__ reqs,
@@ -432,22 +440,24 @@ __global__ __launch_bounds__(256) void lg_cross_attn_mfma(const bf16* __restrict
   constexpr int NS = kLgMfmaSlots;
   constexpr int KS = DH + 8;        // K row stride (elements): rows 16 bytes apart in the banks
   constexpr int VS = NS + 4;        // V^T row stride (elements)
+  constexpr int KH = NS * KS, VH = DH * VS;  // elements per head
   typedef short s16x4 __attribute__((ext_vector_type(4)));
-  __shared__ __attribute__((aligned(16))) bf16 sK[NS * KS];
-  __shared__ __attribute__((aligned(16))) bf16 sV[DH * VS];
+  __shared__ __attribute__((aligned(16))) bf16 sK[kLgMfmaHeads * KH];
+  __shared__ __attribute__((aligned(16))) bf16 sV[kLgMfmaHeads * VH];
   const AttnTile tile = tiles[blockIdx.x];
   if (tile.q_count <= 0) return;
   const AttnReq rq = reqs[tile.req];
-  const int h = tile.head, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int H = g.H;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int qn = lane & 15, kg = lane >> 4;
   const int n_groups = (tile.q_count + 15) / 16;
-  // Q fragments of group gi (features 32 c + 8 kg .. of query qn; zeros past
-  // the tile), and the query's output row
   auto q_row = [&](int gi) {
     const int i = tile.q_begin + 16 * gi + qn;
     return i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
   };
-  auto load_q = [&](int gi, bf16x8(&qf)[NC]) {
+  // Q fragments of (group gi, head h): features 32 c + 8 kg .. of query qn,
+  // zeros past the tile
+  auto load_q = [&](int gi, int h, bf16x8(&qf)[NC]) {
     const bool ok = gi < n_groups && 16 * gi + qn < tile.q_count;
     const int row = ok ? q_row(gi) : 0;
 #pragma unroll
@@ -455,7 +465,7 @@ __global__ __launch_bounds__(256) void lg_cross_attn_mfma(const bf16* __restrict
       qf[c] = ok ? *reinterpret_cast<const bf16x8*>(q + (size_t)row * ldq + h * DH + 32 * c + 8 * kg) : bf16x8{};
   };
   bf16x8 qa[NC], qb[NC];
-  load_q(wave, qa);
+  load_q(wave / H, wave % H, qa);
   const int len = rq.kv_len;
   const int k0 = max(0, len - l_local), p0 = k0 & ~3;
   const bool gpool = gkv != nullptr;
@@ -466,51 +476,49 @@ __global__ __launch_bounds__(256) void lg_cross_attn_mfma(const bf16* __restrict
   const bf16* page0 = pool + (size_t)ptab[pg0] * g.page_elems;
   const bf16* page1 = pool + (size_t)ptab[pg1] * g.page_elems;
   auto page_of = [&](int p) { return p / kPage == pg0 ? page0 : page1; };
-  const int d = g.H * DH;
-  const bf16* grow = gpool ? gkv + (size_t)rq.slot * gkv_ld + (size_t)(2 * dec_layer) * d + h * DH : nullptr;
-  // K pieces (slot e / (DH / 8), features 8 (e % (DH / 8)) ..) and V^T quads
-  // (feature e / 4, slots 4 (e % 4) ..), zeros outside the window
-  for (int e = tid; e < NS * DH / 8; e += 256) {
-    const int j = e / (DH / 8), c = e % (DH / 8), p = p0 + j;
+  const int d = H * DH;
+  const bf16* grow = gpool ? gkv + (size_t)rq.slot * gkv_ld + (size_t)(2 * dec_layer) * d : nullptr;
+  // every head's K pieces (slot j, features 8 c ..) and V^T quads (feature f,
+  // slots 4 u ..), zeros outside the window
+  for (int e = tid; e < H * NS * DH / 8; e += 512) {
+    const int h = e / (NS * DH / 8), r = e % (NS * DH / 8);
+    const int j = r / (DH / 8), c = r % (DH / 8), p = p0 + j;
     bf16x8 v = {};
     if (p >= k0 && p < len)
       v = *reinterpret_cast<const bf16x8*>(page_of(p) + g.k_off(layer_slot, h) + (size_t)(p % kPage) * DH + 8 * c);
     else if (gpool && p == len)
-      v = *reinterpret_cast<const bf16x8*>(grow + 8 * c);
-    *reinterpret_cast<bf16x8*>(sK + j * KS + 8 * c) = v;
+      v = *reinterpret_cast<const bf16x8*>(grow + h * DH + 8 * c);
+    *reinterpret_cast<bf16x8*>(sK + h * KH + j * KS + 8 * c) = v;
   }
-  for (int e = tid; e < DH * NS / 4; e += 256) {
-    const int f = e / 4, pq = p0 + 4 * (e % 4);
+  for (int e = tid; e < H * DH * NS / 4; e += 512) {
+    const int h = e / (DH * NS / 4), r = e % (DH * NS / 4);
+    const int f = r / 4, pq = p0 + 4 * (r % 4);
     bf16x4 v = {};
     if (pq < len)
       v = *reinterpret_cast<const bf16x4*>(page_of(pq) + g.v_off(layer_slot, h) + (size_t)f * kPage + vt_col(pq % kPage));
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      if (pq + r >= len) v[r] = (bf16)0.f;
-      if (gpool && pq + r == len) v[r] = grow[d + f];
+    for (int u = 0; u < 4; ++u) {
+      if (pq + u >= len) v[u] = (bf16)0.f;
+      if (gpool && pq + u == len) v[u] = grow[d + h * DH + f];
     }
-    *reinterpret_cast<bf16x4*>(sV + f * VS + 4 * (e % 4)) = v;
+    *reinterpret_cast<bf16x4*>(sV + h * VH + f * VS + 4 * (r % 4)) = v;
   }
   __syncthreads();
-  // A operands, read from LDS per group (holding them would cost the
-  // registers of two more resident waves per SIMD): K (slot qn, features
-  // 32 c + 8 kg ..) and V^T (feature 16 c + qn, slots 4 kg ..)
-  // (the lane offsets pass through an empty asm per group, so the reads are
-  // not hoisted out of the group loop)
-  const int kofs = qn * KS + 8 * kg, vofs = qn * VS + 4 * kg;
-  int ko = kofs, vo = vofs;
-  auto kfrag = [&](int c) { return *reinterpret_cast<const bf16x8*>(sK + ko + 32 * c); };
-  auto vfrag = [&](int c) { return *reinterpret_cast<const s16x4*>(sV + vo + 16 * VS * c); };
   bool key[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) key[r] = is_key(p0 + 4 * kg + r);
-  auto group = [&](int gi, const bf16x8(&qf)[NC]) {
-    ko = kofs;
-    vo = vofs;
+  // A operands, read from LDS per (group, head): K (slot qn, features
+  // 32 c + 8 kg ..) and V^T (feature 16 c + qn, slots 4 kg ..); the lane
+  // offsets pass through an empty asm so the reads are not hoisted
+  const int kofs = qn * KS + 8 * kg, vofs = qn * VS + 4 * kg;
+  auto work = [&](int gi, int h, const bf16x8(&qf)[NC]) {
+    int ko = kofs + h * KH, vo = vofs + h * VH;
     asm volatile("" : "+v"(ko), "+v"(vo));
     floatx4 sc = {};
 #pragma unroll
-    for (int c = 0; c < NC; ++c) sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kfrag(c), qf[c], sc, 0, 0, 0);
+    for (int c = 0; c < NC; ++c)
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8*>(sK + ko + 32 * c), qf[c], sc,
+                                                   0, 0, 0);
     // sc[r]: slot 4 kg + r of query qn
     float m = -INFINITY;
 #pragma unroll
@@ -534,8 +542,10 @@ __global__ __launch_bounds__(256) void lg_cross_attn_mfma(const bf16* __restrict
 #pragma unroll
     for (int c = 0; c < NO; c += 2) {
       // o0[r], o1[r]: features 16 c + 4 kg + r and 16 (c + 1) + 4 kg + r
-      const floatx4 o0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vfrag(c), pp, floatx4{}, 0, 0, 0);
-      const floatx4 o1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vfrag(c + 1), pp, floatx4{}, 0, 0, 0);
+      const floatx4 o0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+          *reinterpret_cast<const s16x4*>(sV + vo + 16 * VS * c), pp, floatx4{}, 0, 0, 0);
+      const floatx4 o1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+          *reinterpret_cast<const s16x4*>(sV + vo + 16 * VS * (c + 1)), pp, floatx4{}, 0, 0, 0);
       bf16x4 b0, b1;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -559,22 +569,28 @@ __global__ __launch_bounds__(256) void lg_cross_attn_mfma(const bf16* __restrict
       }
     }
   };
-  // groups wave, wave + 4, ...: two at a time, alternating the Q registers
-  for (int gi = wave; gi < n_groups; gi += 8) {
-    load_q(gi + 4, qb);
-    group(gi, qa);
-    if (gi + 4 >= n_groups) break;
-    load_q(gi + 8, qa);
-    group(gi + 4, qb);
+  // (group, head) pair k = 16-query group k / H, head k % H: wave w takes
+  // pairs w, w + 8, ..., so the 8 waves work on 8 consecutive pairs at a
+  // time (with 8 heads, the 8 pieces of the same rows); Q of the wave's
+  // next pair requested first
+  const int n_pairs = n_groups * H;
+  for (int k = wave; k < n_pairs; k += 16) {
+    load_q((k + 8) / H, (k + 8) % H, qb);
+    work(k / H, k % H, qa);
+    if (k + 8 >= n_pairs) break;
+    load_q((k + 16) / H, (k + 16) % H, qa);
+    work((k + 8) / H, (k + 8) % H, qb);
   }
 }
 
 static bool lg_dot_path(bool bf, int l_local, bool gpool) { return bf && l_local + (gpool ? 1 : 0) <= kLgDotKeys; }
 // the window, started at a multiple of 4, and the pooled token within 16 slots
-static bool lg_mfma_path(bool bf, int l_local, bool gpool) {
-  return bf && l_local + (gpool ? 1 : 0) + 3 <= kLgMfmaSlots;
+static bool lg_mfma_path(bool bf, int l_local, bool gpool, int H) {
+  return bf && l_local + (gpool ? 1 : 0) + 3 <= kLgMfmaSlots && H <= kLgMfmaHeads;
 }
-int lg_attention_q_block(bool bf, int l_local, bool gpool) {
+bool lg_attention_all_heads(bool bf, int l_local, bool gpool, int H) { return lg_mfma_path(bf, l_local, gpool, H); }
+int lg_attention_q_block(bool bf, int l_local, bool gpool, int H) {
+  if (lg_mfma_path(bf, l_local, gpool, H)) return kLgMfmaTile;
   return lg_dot_path(bf, l_local, gpool) ? kLgDotTile : kLgQueries;
 }
 
@@ -584,11 +600,11 @@ hipError_t launch_lg_attention(bool bf, const void* q, int ldq, void* out, int l
                                const void* gkv, int gkv_ld, int dec_layer, hipStream_t s) {
   if (n_tiles <= 0) return hipSuccess;
   if (l_local < 1 || l_local > kMaxLocal) return hipErrorInvalidValue;
-  if (q_block != lg_attention_q_block(bf, l_local, gkv != nullptr)) return hipErrorInvalidValue;
+  if (q_block != lg_attention_q_block(bf, l_local, gkv != nullptr, g.H)) return hipErrorInvalidValue;
   const float sl2 = 1.4426950408889634f / sqrtf((float)g.dh);
-  if (lg_mfma_path(bf, l_local, gkv != nullptr)) {
+  if (lg_mfma_path(bf, l_local, gkv != nullptr, g.H)) {
 #define TX_LGM(DH)                                                                                          \
-  lg_cross_attn_mfma<DH><<<n_tiles, 256, 0, s>>>((const bf16*)q, ldq, (bf16*)out, ldo, (const bf16*)pool,          \
+  lg_cross_attn_mfma<DH><<<n_tiles, 512, 0, s>>>((const bf16*)q, ldq, (bf16*)out, ldo, (const bf16*)pool,          \
                                                  page_table, max_pages, g, layer_slot, reqs, tiles, l_local,       \
                                                  (const bf16*)gkv, gkv_ld, dec_layer, sl2)
     switch (g.dh) {
