@@ -12,8 +12,11 @@
 // (the incremental form App. D asks of every cached quantity).
 //
 // Both parts are small next to the decoder GEMMs: the pooling reads the
-// encoded rows once, and the attention touches at most 65 keys per query, so
-// these kernels use plain fp32 arithmetic rather than MFMA tiles.
+// encoded rows once, and the attention touches at most 65 keys per query.
+// The attention is bound by its Q and O rows in HBM: bf16 windows of up to
+// 13 slots run its two small products on matrix cores (lg_cross_attn_mfma),
+// windows of up to 16 keys on v_dot2_f32_bf16 (lg_cross_attn_dot), and the
+// rest (longer windows, fp32 models) in plain fp32 arithmetic.
 #include "tx_internal.h"
 #include "wave_reduce.h"
 
