@@ -73,6 +73,8 @@ CASES = [
     ("dh128-L13-nopool", ModelConfig(256, 2, 1024, 2, 1, rel_pos_buckets=0), 13, False, SHARP, BF16_TOL),
     ("dh64-L13-pool", ModelConfig(256, 4, 512, 2, 2, rel_pos_buckets=16), 13, True, SHARP, BF16_TOL),
     ("dh32-L15-pool", ModelConfig(64, 2, 256, 1, 2, rel_pos_buckets=8), 15, True, SHARP, BF16_TOL),
+    # more heads than the MFMA kernel's blocks serve (8): the dot2 kernel
+    ("dh32-H16-L10-pool", ModelConfig(512, 16, 1024, 1, 2, rel_pos_buckets=8), 10, True, SHARP, BF16_TOL),
     ("dh64-L16-nopool", ModelConfig(256, 4, 512, 2, 1, rel_pos_buckets=0), 16, False, SHARP, BF16_TOL),
     ("dh128-L16-pool", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16), 16, True, SHARP, BF16_TOL),
 ]
