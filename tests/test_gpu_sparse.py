@@ -91,6 +91,23 @@ def test_sparse_ragged(oracle_mod, name, model, l_local, pool, variant, tol):
     _compare(run, oracle_mod.Oracle(m, w), range(wl.B), tol, f"sparse {name}")
 
 
+# Requests with more queries than one tile of the MFMA kernel (288): two
+# full tiles and a partial one, a tile boundary inside the serving tokens,
+# and the serving/candidate split inside a tile; 8 heads, so every wave of a
+# block works (group, head) pairs of its own.
+MULTI_TILE = dict(L=[300, 75, 140], S=[40, 300, 7], C=[600, 12, 281])
+
+
+def test_sparse_multi_tile(oracle_mod):
+    m = _sparse(ModelConfig(256, 8, 1024, 1, 2, rel_pos_buckets=16), 10, True)
+    wl = I.custom_workload(m, cfg_id=43, **MULTI_TILE)
+    w = I.make_weights(m, SHARP)
+    log("sparse multi-tile")
+    run = DeviceCase(wl, w)
+    run.build(range(wl.B))
+    _compare(run, oracle_mod.Oracle(m, w), range(wl.B), BF16_TOL, "sparse multi-tile")
+
+
 def test_global_token_export_vs_oracle(oracle_mod):
     """The pooled token's cross K/V rows against the oracle's, as max |error|
     over rms. Cache rows elsewhere are held to 2e-2 (their own bf16 rounding,
