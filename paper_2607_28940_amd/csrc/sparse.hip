@@ -423,9 +423,11 @@ __global__ __launch_bounds__(4 * kLgDotQueries) void lg_cross_attn_dot(const bf1
 // in blocks of their own, the 256-byte pieces of a row went to memory far
 // apart in time, and the launch ran at the ~4 TB/s such a sweep gets). The output accumulator holds 4
 // features of one query per lane and 16-feature chunk; two row swaps per
-// pair of chunks leave each lane 8 consecutive features, so every 16-byte
-// store covers 64 contiguous bytes of a row per query, as do the Q loads
-// (the B operand: 8 consecutive features per lane).
+// pair of chunks leave each lane 8 consecutive features (64 contiguous
+// bytes of a row per query over the four key groups, as the Q loads read:
+// the B operand takes 8 consecutive features per lane), and a rotation by 8
+// lanes pairs two such halves, so that each store writes whole 128-byte
+// lines of 8 queries.
 constexpr int kLgMfmaSlots = 16;
 constexpr int kLgMfmaTile = 288;   // queries per tile
 constexpr int kLgMfmaHeads = 8;    // heads per block (the model's, at most)
@@ -454,15 +456,16 @@ __global__ __launch_bounds__(512) void lg_cross_attn_mfma(const bf16* __restrict
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int qn = lane & 15, kg = lane >> 4;
   const int n_groups = (tile.q_count + 15) / 16;
-  auto q_row = [&](int gi) {
-    const int i = tile.q_begin + 16 * gi + qn;
+  // token row of query j of 16-query group gi
+  auto row_of = [&](int gi, int j) {
+    const int i = tile.q_begin + 16 * gi + j;
     return i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
   };
   // Q fragments of (group gi, head h): features 32 c + 8 kg .. of query qn,
   // zeros past the tile
   auto load_q = [&](int gi, int h, bf16x8(&qf)[NC]) {
     const bool ok = gi < n_groups && 16 * gi + qn < tile.q_count;
-    const int row = ok ? q_row(gi) : 0;
+    const int row = ok ? row_of(gi, qn) : 0;
 #pragma unroll
     for (int c = 0; c < NC; ++c)
       qf[c] = ok ? *reinterpret_cast<const bf16x8*>(q + (size_t)row * ldq + h * DH + 32 * c + 8 * kg) : bf16x8{};
@@ -540,10 +543,8 @@ __global__ __launch_bounds__(512) void lg_cross_attn_mfma(const bf16* __restrict
     l = xor32_sum(row16_sum(l));
     const float inv = 1.f / l;
     const s16x4 pp = __builtin_bit_cast(s16x4, pb);
-    const bool ok = 16 * gi + qn < tile.q_count;
-    const int row = ok ? q_row(gi) : 0;
-#pragma unroll
-    for (int c = 0; c < NO; c += 2) {
+    // features 16 c .. 16 c + 31 of query qn: 8 consecutive ones per key group
+    auto out_chunks = [&](int c) {
       // o0[r], o1[r]: features 16 c + 4 kg + r and 16 (c + 1) + 4 kg + r
       const floatx4 o0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
           *reinterpret_cast<const s16x4*>(sV + vo + 16 * VS * c), pp, floatx4{}, 0, 0, 0);
@@ -566,9 +567,43 @@ __global__ __launch_bounds__(512) void lg_cross_attn_mfma(const bf16* __restrict
         x[w] = b[0];
         y[w] = b[1];
       }
-      if (ok) {
-        const u32x4_t unit = {x[0], x[1], y[0], y[1]};
-        *reinterpret_cast<u32x4_t*>(out + (size_t)row * ldo + h * DH + 16 * c + 8 * kg) = unit;
+      return u32x4_t{x[0], x[1], y[0], y[1]};
+    };
+    if constexpr (DH % 64 == 0) {
+      // Whole 128-byte lines per store: features 16 c .. 16 c + 63 of a
+      // query are e0 (first half) and e1 (second half) of its four lanes.
+      // Rotating e1 by 8 lanes within each row of 16 puts the second half of
+      // query j next to the first half of query j + 8 or j - 8, so a store
+      // serves queries 0..7 (a) or 8..15 (b) with whole lines: query
+      // (qn & 7) (+ 8 for b), features 16 c + 8 kg, + 32 where the lane took
+      // the rotated half. A store of half lines from 16 queries costs ~15% of
+      // the kernel's time.
+      const int j = qn & 7;
+      const bool lo = qn < 8;
+      const bool ok_a = 16 * gi + j < tile.q_count, ok_b = 16 * gi + j + 8 < tile.q_count;
+      const int row_a = ok_a ? row_of(gi, j) : 0, row_b = ok_b ? row_of(gi, j + 8) : 0;
+#pragma unroll
+      for (int c = 0; c < NO; c += 4) {
+        const u32x4_t e0 = out_chunks(c), e1 = out_chunks(c + 2);
+        u32x4_t a, b;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const uint32_t r = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)e1[w], 0x128 /* row_ror:8 */, 0xf, 0xf, false);
+          a[w] = lo ? e0[w] : r;
+          b[w] = lo ? r : e0[w];
+        }
+        const int col = h * DH + 16 * c + 8 * kg;
+        if (ok_a) *reinterpret_cast<u32x4_t*>(out + (size_t)row_a * ldo + col + (lo ? 0 : 32)) = a;
+        if (ok_b) *reinterpret_cast<u32x4_t*>(out + (size_t)row_b * ldo + col + (lo ? 32 : 0)) = b;
+      }
+    } else {
+      // a head piece of 32 features is half a line, whichever lanes hold it
+      const bool ok = 16 * gi + qn < tile.q_count;
+      const int row = ok ? row_of(gi, qn) : 0;
+#pragma unroll
+      for (int c = 0; c < NO; c += 2) {
+        const u32x4_t e = out_chunks(c);
+        if (ok) *reinterpret_cast<u32x4_t*>(out + (size_t)row * ldo + h * DH + 16 * c + 8 * kg) = e;
       }
     }
   };

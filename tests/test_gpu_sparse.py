@@ -76,6 +76,7 @@ CASES = [
     # more heads than the MFMA kernel's blocks serve (8): the dot2 kernel
     ("dh32-H16-L10-pool", ModelConfig(512, 16, 1024, 1, 2, rel_pos_buckets=8), 10, True, SHARP, BF16_TOL),
     ("dh64-L16-nopool", ModelConfig(256, 4, 512, 2, 1, rel_pos_buckets=0), 16, False, SHARP, BF16_TOL),
+    ("dh128-L14-nopool", ModelConfig(256, 2, 1024, 2, 1, rel_pos_buckets=0), 14, False, SHARP, BF16_TOL),
     ("dh128-L16-pool", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16), 16, True, SHARP, BF16_TOL),
 ]
 
@@ -94,18 +95,26 @@ def test_sparse_ragged(oracle_mod, name, model, l_local, pool, variant, tol):
 # Requests with more queries than one tile of the MFMA kernel (288): two
 # full tiles and a partial one, a tile boundary inside the serving tokens,
 # and the serving/candidate split inside a tile; 8 heads, so every wave of a
-# block works (group, head) pairs of its own.
+# block works (group, head) pairs of its own. The same requests on the dot2
+# kernel (windows of 14 and 15 keys): several passes of 128 queries per
+# request, odd query counts (the last pair of queries half out of the tile).
 MULTI_TILE = dict(L=[300, 75, 140], S=[40, 300, 7], C=[600, 12, 281])
+MULTI_TILE_CASES = [
+    ("mfma-dh128-H8-L10-pool", ModelConfig(256, 8, 1024, 1, 2, rel_pos_buckets=16), 10, True),
+    ("dot-dh128-L14-pool", ModelConfig(256, 2, 1024, 1, 2, rel_pos_buckets=16), 14, True),
+    ("dot-dh64-L15-nopool", ModelConfig(256, 4, 512, 1, 2, rel_pos_buckets=0), 15, False),
+]
 
 
-def test_sparse_multi_tile(oracle_mod):
-    m = _sparse(ModelConfig(256, 8, 1024, 1, 2, rel_pos_buckets=16), 10, True)
+@pytest.mark.parametrize("name,model,l_local,pool", MULTI_TILE_CASES, ids=[c[0] for c in MULTI_TILE_CASES])
+def test_sparse_multi_tile(oracle_mod, name, model, l_local, pool):
+    m = _sparse(model, l_local, pool)
     wl = I.custom_workload(m, cfg_id=43, **MULTI_TILE)
     w = I.make_weights(m, SHARP)
-    log("sparse multi-tile")
+    log(f"sparse multi-tile {name}")
     run = DeviceCase(wl, w)
     run.build(range(wl.B))
-    _compare(run, oracle_mod.Oracle(m, w), range(wl.B), BF16_TOL, "sparse multi-tile")
+    _compare(run, oracle_mod.Oracle(m, w), range(wl.B), BF16_TOL, f"sparse multi-tile {name}")
 
 
 def test_global_token_export_vs_oracle(oracle_mod):
