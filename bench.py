@@ -20,7 +20,11 @@ comes from HIP events the library records around its launches on the stream
 during the timed steps (tx_profile_*: a few untimed steps with every launch
 bracketed pick that kernel and give the per-class table first), the minimum,
 median and maximum of the timed steps' own times, and the fp64 CPU oracle's
-own throughput on a bounded sample.
+own throughput on a bounded sample. The per-class table ("kernels") gives
+every kernel class's average launch time in those untimed steps, its
+algorithmic TFLOP/s and GB/s, and the fraction of the roof that bounds it
+(above the ridge of the dtype's arithmetic peak over 8 TB/s: bf16 MFMA, or
+the fp32 vector ALUs for fp32 models; HBM below).
 """
 from __future__ import annotations
 
@@ -283,19 +287,25 @@ def main():
     tflops = work["flop"] / (ms / 1e3) / 1e12
     peak = PEAK_BF16_TFLOPS if m.dtype == "bf16" else PEAK_FP32_TFLOPS
 
+    ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)  # flop per byte where the two roofs meet
+    arith = "mfma" if m.dtype == "bf16" else "alu"  # fp32 models run on the vector ALUs
     kernels = {}
     for name, p in prof_all.items():
         avg = p["ms"] / p["launches"]
+        tf = p["flops"] / (p["ms"] / 1e3) / 1e12 if p["flops"] else None
+        gbs = p["bytes"] / (p["ms"] / 1e3) / 1e9
+        on_mfma = bool(p["flops"]) and p["flops"] / max(p["bytes"], 1) > ridge
         kernels[name] = {"avg_ms": round(avg, 5), "launches_per_step": p["launches"] / args.profile_steps,
                          "share": round(p["ms"] / (ms * args.profile_steps), 4),
-                         "tflops": round(p["flops"] / (p["ms"] / 1e3) / 1e12, 2) if p["flops"] else None,
-                         "gbs": round(p["bytes"] / (p["ms"] / 1e3) / 1e9, 1)}
+                         "tflops": round(tf, 2) if tf is not None else None, "gbs": round(gbs, 1),
+                         "bound": arith if on_mfma else "hbm",
+                         "frac": round(tf / peak if on_mfma else gbs / PEAK_HBM_GBS, 4)}
     roofline = None
     if prof.get(dom, {}).get("launches"):
         p = prof[dom]
         avg_s = p["ms"] / p["launches"] / 1e3
         fl_launch, by_launch = p["flops"] / p["launches"], p["bytes"] / p["launches"]
-        mfma = fl_launch > 0 and fl_launch / max(by_launch, 1) > peak * 1e12 / (PEAK_HBM_GBS * 1e9)
+        mfma = fl_launch > 0 and fl_launch / max(by_launch, 1) > ridge
         # the counters were taken on the default headline run: other
         # workloads and modes launch the same kernel on other shapes
         default_run = (args.workload == "headline" and not args.append and not args.events and not args.actions
@@ -303,7 +313,7 @@ def main():
         traffic = measured_traffic(args.traffic_json, dom) if default_run else None
         if mfma:
             ach = fl_launch / avg_s / 1e12
-            roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
+            roofline = {"kernel": dom, "bound": arith, "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
                         "frac": round(ach / peak, 4), "traffic": traffic,
                         "per_launch": {"flop": fl_launch, "bytes": by_launch, "avg_ms": round(avg_s * 1e3, 5)}}
         else:
