@@ -324,7 +324,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        n_cpu = args.cpu_requests or (32 if m.l_local > 0 else 4)
+        n_cpu = args.cpu_requests or (32 if m.l_local > 0 else 10)  # ~10 s of the oracle on 16 cores
         cpu = cpu_baseline(wl, weights, min(n_cpu, wl.B))
 
     sparse = m.l_local > 0
