@@ -1207,9 +1207,10 @@ int run_score_pass(const tx_kv_cache* c, const int32_t* ids, const int64_t* kvle
     mx = std::max<int64_t>(mx, S + C);
   }
   const bool sparse = m->l_local > 0;
-  const int qb = sparse ? lg_attention_q_block(bf, m->l_local, m->gpool, H) : paged_attention_q_block(bf, m->dh);
-  // heads per tile group: one tile serves every head on the sparse MFMA kernel
-  const int th = sparse && lg_attention_all_heads(bf, m->l_local, m->gpool, H) ? 1 : H;
+  const int qb =
+      sparse ? lg_attention_q_block(bf, m->l_local, m->gpool, H, m->dh) : paged_attention_q_block(bf, m->dh);
+  // head groups of the tile plan: a sparse MFMA tile serves several heads
+  const int th = sparse ? H / lg_attention_heads_per_tile(bf, m->l_local, m->gpool, H, m->dh) : H;
   const int sqb = self_attention_q_block(bf, m->dh);
   std::vector<AttnTile> t_full, t_cand;
   std::vector<SelfTile> s_full, s_cand;

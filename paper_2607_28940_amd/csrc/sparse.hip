@@ -13,10 +13,9 @@
 //
 // Both parts are small next to the decoder GEMMs: the pooling reads the
 // encoded rows once, and the attention touches at most 65 keys per query.
-// The attention is bound by its Q and O rows in HBM: bf16 windows of up to
-// 13 slots run its two small products on matrix cores (lg_cross_attn_mfma),
-// windows of up to 16 keys on v_dot2_f32_bf16 (lg_cross_attn_dot), and the
-// rest (longer windows, fp32 models) in plain fp32 arithmetic.
+// The attention is bound by its Q and O rows in HBM: bf16 models run its two
+// small products on matrix cores (lg_cross_attn_mfma), fp32 models in plain
+// fp32 arithmetic (lg_cross_attn).
 #include "tx_internal.h"
 #include "wave_reduce.h"
 
@@ -214,198 +213,20 @@ __global__ __launch_bounds__(256) void lg_cross_attn(const T* __restrict__ q, in
   for (int e = 0; e < DP; ++e) out[(size_t)row * ldo + h * DH + part * DP + e] = (T)(acc[e] * inv);
 }
 
-// bf16 models with at most 16 keys per query (l_local <= 15 with the global
-// token, l_local <= 16 without; the paper's setting is 10 + 1): the keys and
-// values stay bf16 in LDS and both products run on v_dot2_f32_bf16 (two
-// bf16 products per instruction, fp32 accumulation). Four lanes serve a
-// query; lane `part` owns the 8-feature pieces part, part + 4, ... of the
-// head, so each 16-byte load or store of Q and O covers 64 contiguous bytes
-// of a row per query. The query's Q pieces are requested before the block
-// stages its keys, so their latency overlaps the staging.
-// Keys are staged in slots of pairs aligned to even cache positions: pair a
-// holds positions 2 (a0 + a) and 2 (a0 + a) + 1, which sit side by side in a
-// page's V^T slab (the slab's column permutation keeps even-odd neighbours
-// together), so one 4-byte load fetches both values of a feature. Window
-// positions below k0 or at len and above are masked (their K rows are zero in
-// LDS; a V value at len is the zero the page scatter keeps past a request's
-// length, and the one below k0 is a valid cached value times probability 0).
-// The pooled token takes the pair after the window, with a zero partner. All
-// of a query's scores are formed first (in registers), then the softmax, then
-// PV over the pairs, one dot2 per pair and feature, with the probabilities
-// rounded to bf16 (as the dense kernels round P) and l summed over the
-// rounded values.
-// A block serves every query of its (request, head), 128 at a time, so the
-// window is staged once per (request, head): a page's V^T slab holds one
-// 128-byte line per feature, and a window's values, 4 KB of them, touch 128
-// such lines per head (staged per 128 queries, those line reads took a fifth
-// of the launch). The next 128 queries' Q pieces are requested before the
-// current ones are worked on.
-constexpr int kLgDotKeys = 16;
-constexpr int kLgDotQueries = 128;  // queries per pass of a block (4 lanes each)
-constexpr int kLgDotTile = 1 << 20;  // queries per tile: the whole request
-constexpr int kLgQueries = 64;      // queries per block of the general kernel
-constexpr int kLgDotPairs = kLgDotKeys / 2 + 2;  // window + alignment + pooled token
+constexpr int kLgQueries = 64;  // queries per block of the general kernel
 
-template <int DH>
-__global__ __launch_bounds__(4 * kLgDotQueries) void lg_cross_attn_dot(const bf16* __restrict__ q, int ldq, bf16* __restrict__ out,
-                                                         int ldo, const bf16* __restrict__ pool,
-                                                         const int32_t* __restrict__ page_table, int max_pages,
-                                                         PageGeom g, int layer_slot, const AttnReq* __restrict__ reqs,
-                                                         const AttnTile* __restrict__ tiles, int l_local,
-                                                         const bf16* __restrict__ gkv, int gkv_ld, int dec_layer,
-                                                         float scale_log2) {
-  constexpr int NP = DH / 32;  // pieces per lane
-  constexpr int MP = kLgDotPairs, MS = 2 * MP;
-  __shared__ __attribute__((aligned(16))) bf16 sK[MS * DH];
-  __shared__ __attribute__((aligned(16))) uint32_t sV[MP * DH];
-  const AttnTile tile = tiles[blockIdx.x];
-  if (tile.q_count <= 0) return;
-  const AttnReq rq = reqs[tile.req];
-  const int h = tile.head, tid = threadIdx.x, part = tid & 3;
-  // the Q pieces of query q_begin + qc + tid / 4, when the tile has it
-  auto q_row = [&](int qc) {
-    const int i = tile.q_begin + qc + (tid >> 2);
-    return i < rq.qa_n ? rq.qa_row + i : rq.qb_row + (i - rq.qa_n);
-  };
-  auto load_q = [&](int qc, bf16x8(&qv)[NP]) {
-    if (qc + (tid >> 2) < tile.q_count) {
-      const int row = q_row(qc);
-#pragma unroll
-      for (int e = 0; e < NP; ++e)
-        qv[e] = *reinterpret_cast<const bf16x8*>(q + (size_t)row * ldq + h * DH + (e * 4 + part) * 8);
-    }
-  };
-  // the first 128 queries' Q pieces, requested first
-  bf16x8 qv[NP], qn[NP];
-  load_q(0, qv);
-  const int len = rq.kv_len;
-  const int k0 = max(0, len - l_local);
-  const int a0 = k0 >> 1, npl = ((len - 1) >> 1) - a0 + 1;  // local pairs
-  const int np = npl + (gkv ? 1 : 0);
-  const int p0 = 2 * a0;  // position of slot 0
-  // the window's (at most two) pages, as scalars
-  const int32_t* ptab = page_table + (size_t)rq.slot * max_pages;
-  const int pg_lo = p0 / kPage, pg_hi = (2 * (a0 + npl) - 1) / kPage;
-  const bf16* page_lo = pool + (size_t)ptab[pg_lo] * g.page_elems;
-  const bf16* page_hi = pool + (size_t)ptab[pg_hi] * g.page_elems;
-  const int d = g.H * DH;
-  const bf16* gk = gkv ? gkv + (size_t)rq.slot * gkv_ld + (size_t)(2 * dec_layer) * d + h * DH : nullptr;
-  // K rows of every slot, 16 bytes per thread and step
-  for (int e = tid; e < 2 * np * (DH / 8); e += 4 * kLgDotQueries) {
-    const int j = e / (DH / 8), c = e % (DH / 8);
-    bf16x8 v = {};
-    if (j < 2 * npl) {
-      const int pos = p0 + j;
-      if (pos >= k0 && pos < len) {
-        const bf16* pg = pos / kPage == pg_lo ? page_lo : page_hi;
-        v = *reinterpret_cast<const bf16x8*>(pg + g.k_off(layer_slot, h) + (size_t)(pos % kPage) * DH + c * 8);
-      }
-    } else if (j == 2 * npl) {
-      v = *reinterpret_cast<const bf16x8*>(gk + c * 8);
-    }
-    *reinterpret_cast<bf16x8*>(sK + j * DH + c * 8) = v;
-  }
-  // V pairs: one 4-byte word of the V^T slab per pair and feature
-  for (int e = tid; e < np * DH; e += 4 * kLgDotQueries) {
-    const int a = e / DH, f = e % DH;
-    uint32_t w;
-    if (a < npl) {
-      const int pos = p0 + 2 * a;
-      const bf16* pg = pos / kPage == pg_lo ? page_lo : page_hi;
-      w = *reinterpret_cast<const uint32_t*>(pg + g.v_off(layer_slot, h) + (size_t)f * kPage + vt_col(pos % kPage));
-    } else {
-      const bf16x2 v2 = {gk[d + f], (bf16)0.f};
-      w = __builtin_bit_cast(uint32_t, v2);
-    }
-    sV[a * DH + f] = w;
-  }
-  __syncthreads();
-  // slot j is a key unless it lies outside the window (slot 0 below k0, the
-  // window's last slot at len) or is the pooled token's zero partner
-  auto is_key = [&](int j) {
-    if (j >= 2 * np) return false;
-    if (j < 2 * npl) return p0 + j >= k0 && p0 + j < len;
-    return j == 2 * npl;
-  };
-  for (int qc = 0; qc < tile.q_count; qc += kLgDotQueries) {
-    if (qc + kLgDotQueries < tile.q_count) load_q(qc + kLgDotQueries, qn);
-    if (qc + (tid >> 2) < tile.q_count) {
-      float s[MS];
-      float m = -INFINITY;
-#pragma unroll
-      for (int j = 0; j < MS; ++j) {
-        s[j] = -INFINITY;
-        if (is_key(j)) {
-          float acc = 0.f;
-#pragma unroll
-          for (int e = 0; e < NP; ++e) {
-            const bf16x8 k8 = *reinterpret_cast<const bf16x8*>(sK + j * DH + (e * 4 + part) * 8);
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-              acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{qv[e][2 * c], qv[e][2 * c + 1]},
-                                                    bf16x2{k8[2 * c], k8[2 * c + 1]}, acc, false);
-          }
-          s[j] = quad_sum(acc) * scale_log2;
-          m = fmaxf(m, s[j]);
-        }
-      }
-      bf16 pb[MS];
-      float l = 0.f;
-#pragma unroll
-      for (int j = 0; j < MS; ++j) {
-        pb[j] = (bf16)__builtin_amdgcn_exp2f(s[j] - m);  // 0 where masked
-        l += (float)pb[j];
-      }
-      float o[NP][8];
-#pragma unroll
-      for (int e = 0; e < NP; ++e)
-#pragma unroll
-        for (int c = 0; c < 8; ++c) o[e][c] = 0.f;
-#pragma unroll
-      for (int a = 0; a < MP; ++a) {
-        if (a < np) {
-          const bf16x2 pp = {pb[2 * a], pb[2 * a + 1]};
-#pragma unroll
-          for (int e = 0; e < NP; ++e) {
-            // features (e * 4 + part) * 8 .. + 7 of the pair, 16 bytes per 4
-            // features (taken apart element-wise: this compiler folds a
-            // bit_cast of u32 vector element c to element 0)
-            const bf16* vr = reinterpret_cast<const bf16*>(sV + a * DH + (e * 4 + part) * 8);
-            const bf16x8 v0 = *reinterpret_cast<const bf16x8*>(vr);
-            const bf16x8 v1 = *reinterpret_cast<const bf16x8*>(vr + 8);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-              o[e][c] = __builtin_amdgcn_fdot2_f32_bf16(pp, bf16x2{v0[2 * c], v0[2 * c + 1]}, o[e][c], false);
-              o[e][4 + c] = __builtin_amdgcn_fdot2_f32_bf16(pp, bf16x2{v1[2 * c], v1[2 * c + 1]}, o[e][4 + c], false);
-            }
-          }
-        }
-      }
-      const float inv = 1.f / l;
-      const int row = q_row(qc);
-#pragma unroll
-      for (int e = 0; e < NP; ++e) {
-        bf16x8 w;
-#pragma unroll
-        for (int c = 0; c < 8; ++c) w[c] = (bf16)(o[e][c] * inv);
-        *reinterpret_cast<bf16x8*>(out + (size_t)row * ldo + h * DH + (e * 4 + part) * 8) = w;
-      }
-    }
-#pragma unroll
-    for (int e = 0; e < NP; ++e) qv[e] = qn[e];
-  }
-}
-
-// The same windows on matrix cores, for windows that fit 16 key slots after
-// their start is rounded down to a multiple of 4 (l_local + 1 <= 13 with the
-// pooled token, the paper's 10 + 1 included). Every query of a
-// (request, head) sees the same keys, so per group of 16 queries the scores
-// are one small product S^T = K Q^T (v_mfma_f32_16x16x32_bf16, keys as rows:
-// lane (q, g) ends with slots 4 g .. 4 g + 3 of query q) and the output one
-// more, O^T = V^T P^T (v_mfma_f32_16x16x16_bf16), whose P^T operand wants
-// exactly that layout: four slots of one query per lane. The softmax runs in
-// the accumulator registers (row maximum and sum over the query's four lanes
-// by row swaps), and no value changes lanes between the two products.
+// The same windows on matrix cores, for every bf16 model: NS key slots
+// (16, 32, ..., 80) hold the window after its start is rounded down to a
+// multiple of 4, plus the pooled token (NS = 16 for the paper's 10 + 1).
+// Every query of a (request, head) sees the same keys, so per group of 16
+// queries and 16 slots the scores are one small product S^T = K Q^T
+// (v_mfma_f32_16x16x32_bf16, keys as rows: lane (q, g) ends with slots
+// 4 g .. 4 g + 3 of the chunk for query q) and the output is a sum of more,
+// O^T = V^T P^T over the chunks (v_mfma_f32_16x16x16_bf16), whose P^T
+// operand wants exactly that layout: four slots of one query per lane. The
+// softmax runs in the accumulator registers (row maximum and sum over the
+// query's four lanes by row swaps), and no value changes lanes between the
+// two products.
 // Slot j is cache position p0 + j with p0 = k0 rounded down to a multiple of
 // 4, and the pooled token takes the slot of position len; four slots are
 // four consecutive positions, which a page's V^T slab keeps side by side (its
@@ -413,46 +234,60 @@ __global__ __launch_bounds__(4 * kLgDotQueries) void lg_cross_attn_dot(const bf1
 // staged in 8-byte quads and K in 16-byte row pieces. Slots outside the
 // window are masked and staged as zeros (nothing past the request's cached
 // positions is read), so stale or poisoned page contents cannot reach the
-// result.
-// A block serves up to kLgMfmaTile queries of one request for every head:
-// it stages the windows of all heads once, and its 8 waves take (group of
-// 16 queries, head) pairs eight consecutive ones at a time (with 8 heads, the
-// 8 head pieces of the same 16 rows), the next pair's Q fragments requested
-// before the current one is worked on. So each query's Q row is read, and
-// its O row written, as a whole 2 KB row within a short span (head by head
-// in blocks of their own, the 256-byte pieces of a row went to memory far
-// apart in time, and the launch ran at the ~4 TB/s such a sweep gets). The output accumulator holds 4
-// features of one query per lane and 16-feature chunk; two row swaps per
-// pair of chunks leave each lane 8 consecutive features (64 contiguous
+// result. The slots that hold cached positions (at most 64 + 3 from a
+// multiple of 4) span at most two pages.
+// A block serves a tile of queries of one request for hb heads (all of them
+// at the paper's window: 8 heads of 16 slots fit 74 KB of LDS; fewer for
+// longer windows, hb a divisor of H): it stages those heads' windows once,
+// and its 8 waves take (group of 16 queries, head) pairs eight consecutive
+// ones at a time (with 8 heads, the 8 head pieces of the same 16 rows), the
+// next pair's Q fragments requested before the current one is worked on. So
+// each query's Q row is read, and its O row written, as whole rows or
+// pieces of hb heads within a short span (head by head in blocks of their
+// own, the 256-byte pieces of a row went to memory far apart in time, and
+// the launch ran at the ~4 TB/s such a sweep gets). The output accumulator
+// holds 4 features of one query per lane and 16-feature chunk; two row swaps
+// per pair of chunks leave each lane 8 consecutive features (64 contiguous
 // bytes of a row per query over the four key groups, as the Q loads read:
 // the B operand takes 8 consecutive features per lane), and a rotation by 8
 // lanes pairs two such halves, so that each store writes whole 128-byte
 // lines of 8 queries.
-constexpr int kLgMfmaSlots = 16;
-constexpr int kLgMfmaTile = 288;   // queries per tile
-constexpr int kLgMfmaHeads = 8;    // heads per block (the model's, at most)
+constexpr int kLgMfmaMaxSlots = 80;
+constexpr int kLgMfmaPairs = 144;  // (16-query group, head) pairs per tile
+constexpr int kLgMfmaLds = 77824;  // LDS budget of a block's windows (76 KB: two blocks per CU)
 
-template <int DH>
+// LDS bytes of one head's window: K rows of DH + 8 elements, V^T rows of NS + 4
+constexpr int lg_head_bytes(int ns, int dh) { return 2 * (ns * (dh + 8) + dh * (ns + 4)); }
+// heads a block's LDS holds: the largest power of two up to 8 within the budget
+constexpr int lg_max_heads(int ns, int dh) {
+  return 8 * lg_head_bytes(ns, dh) <= kLgMfmaLds   ? 8
+         : 4 * lg_head_bytes(ns, dh) <= kLgMfmaLds ? 4
+         : 2 * lg_head_bytes(ns, dh) <= kLgMfmaLds ? 2
+                                                   : 1;
+}
+
+template <int DH, int NS>
 __global__ __launch_bounds__(512) void lg_cross_attn_mfma(const bf16* __restrict__ q, int ldq, bf16* __restrict__ out,
                                                           int ldo, const bf16* __restrict__ pool,
                                                           const int32_t* __restrict__ page_table, int max_pages,
                                                           PageGeom g, int layer_slot, const AttnReq* __restrict__ reqs,
-                                                          const AttnTile* __restrict__ tiles, int l_local,
+                                                          const AttnTile* __restrict__ tiles, int l_local, int hb,
                                                           const bf16* __restrict__ gkv, int gkv_ld, int dec_layer,
                                                           float scale_log2) {
   constexpr int NC = DH / 32;       // k chunks of the score product
   constexpr int NO = DH / 16;       // feature chunks of the output product
-  constexpr int NS = kLgMfmaSlots;
+  constexpr int NCH = NS / 16;      // slot chunks
   constexpr int KS = DH + 8;        // K row stride (elements): rows 16 bytes apart in the banks
   constexpr int VS = NS + 4;        // V^T row stride (elements)
   constexpr int KH = NS * KS, VH = DH * VS;  // elements per head
+  constexpr int HB = lg_max_heads(NS, DH);
   typedef short s16x4 __attribute__((ext_vector_type(4)));
-  __shared__ __attribute__((aligned(16))) bf16 sK[kLgMfmaHeads * KH];
-  __shared__ __attribute__((aligned(16))) bf16 sV[kLgMfmaHeads * VH];
+  __shared__ __attribute__((aligned(16))) bf16 sK[HB * KH];
+  __shared__ __attribute__((aligned(16))) bf16 sV[HB * VH];
   const AttnTile tile = tiles[blockIdx.x];
   if (tile.q_count <= 0) return;
   const AttnReq rq = reqs[tile.req];
-  const int H = g.H;
+  const int h0 = tile.head * hb;  // the tile's first head
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int qn = lane & 15, kg = lane >> 4;
   const int n_groups = (tile.q_count + 15) / 16;
@@ -471,7 +306,7 @@ __global__ __launch_bounds__(512) void lg_cross_attn_mfma(const bf16* __restrict
       qf[c] = ok ? *reinterpret_cast<const bf16x8*>(q + (size_t)row * ldq + h * DH + 32 * c + 8 * kg) : bf16x8{};
   };
   bf16x8 qa[NC], qb[NC];
-  load_q(wave / H, wave % H, qa);
+  load_q(wave / hb, h0 + wave % hb, qa);
   const int len = rq.kv_len;
   const int k0 = max(0, len - l_local), p0 = k0 & ~3;
   const bool gpool = gkv != nullptr;
@@ -482,74 +317,91 @@ __global__ __launch_bounds__(512) void lg_cross_attn_mfma(const bf16* __restrict
   const bf16* page0 = pool + (size_t)ptab[pg0] * g.page_elems;
   const bf16* page1 = pool + (size_t)ptab[pg1] * g.page_elems;
   auto page_of = [&](int p) { return p / kPage == pg0 ? page0 : page1; };
-  const int d = H * DH;
+  const int d = g.H * DH;
   const bf16* grow = gpool ? gkv + (size_t)rq.slot * gkv_ld + (size_t)(2 * dec_layer) * d : nullptr;
-  // every head's K pieces (slot j, features 8 c ..) and V^T quads (feature f,
+  // the heads' K pieces (slot j, features 8 c ..) and V^T quads (feature f,
   // slots 4 u ..), zeros outside the window
-  for (int e = tid; e < H * NS * DH / 8; e += 512) {
-    const int h = e / (NS * DH / 8), r = e % (NS * DH / 8);
+  for (int e = tid; e < hb * NS * DH / 8; e += 512) {
+    const int hl = e / (NS * DH / 8), r = e % (NS * DH / 8), h = h0 + hl;
     const int j = r / (DH / 8), c = r % (DH / 8), p = p0 + j;
     bf16x8 v = {};
     if (p >= k0 && p < len)
       v = *reinterpret_cast<const bf16x8*>(page_of(p) + g.k_off(layer_slot, h) + (size_t)(p % kPage) * DH + 8 * c);
     else if (gpool && p == len)
       v = *reinterpret_cast<const bf16x8*>(grow + h * DH + 8 * c);
-    *reinterpret_cast<bf16x8*>(sK + h * KH + j * KS + 8 * c) = v;
+    *reinterpret_cast<bf16x8*>(sK + hl * KH + j * KS + 8 * c) = v;
   }
-  for (int e = tid; e < H * DH * NS / 4; e += 512) {
-    const int h = e / (DH * NS / 4), r = e % (DH * NS / 4);
-    const int f = r / 4, pq = p0 + 4 * (r % 4);
+  for (int e = tid; e < hb * DH * NS / 4; e += 512) {
+    const int hl = e / (DH * NS / 4), r = e % (DH * NS / 4), h = h0 + hl;
+    const int f = r / (NS / 4), u = r % (NS / 4), pq = p0 + 4 * u;
     bf16x4 v = {};
     if (pq < len)
       v = *reinterpret_cast<const bf16x4*>(page_of(pq) + g.v_off(layer_slot, h) + (size_t)f * kPage + vt_col(pq % kPage));
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      if (pq + u >= len) v[u] = (bf16)0.f;
-      if (gpool && pq + u == len) v[u] = grow[d + h * DH + f];
+    for (int t = 0; t < 4; ++t) {
+      if (pq + t >= len) v[t] = (bf16)0.f;
+      if (gpool && pq + t == len) v[t] = grow[d + h * DH + f];
     }
-    *reinterpret_cast<bf16x4*>(sV + h * VH + f * VS + 4 * (r % 4)) = v;
+    *reinterpret_cast<bf16x4*>(sV + hl * VH + f * VS + 4 * u) = v;
   }
   __syncthreads();
-  bool key[4];
+  bool key[NCH][4];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) key[r] = is_key(p0 + 4 * kg + r);
-  // A operands, read from LDS per (group, head): K (slot qn, features
-  // 32 c + 8 kg ..) and V^T (feature 16 c + qn, slots 4 kg ..); the lane
-  // offsets pass through an empty asm so the reads are not hoisted
+  for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) key[ch][r] = is_key(p0 + 16 * ch + 4 * kg + r);
+  // A operands, read from LDS per (group, head): K (slot 16 ch + qn,
+  // features 32 c + 8 kg ..) and V^T (feature 16 c + qn, slots
+  // 16 ch + 4 kg ..); the lane offsets pass through an empty asm so the
+  // reads are not hoisted
   const int kofs = qn * KS + 8 * kg, vofs = qn * VS + 4 * kg;
-  auto work = [&](int gi, int h, const bf16x8(&qf)[NC]) {
-    int ko = kofs + h * KH, vo = vofs + h * VH;
+  auto work = [&](int gi, int hl, const bf16x8(&qf)[NC]) {
+    int ko = kofs + hl * KH, vo = vofs + hl * VH;
     asm volatile("" : "+v"(ko), "+v"(vo));
-    floatx4 sc = {};
+    floatx4 sc[NCH];
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
-      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8*>(sK + ko + 32 * c), qf[c], sc,
-                                                   0, 0, 0);
-    // sc[r]: slot 4 kg + r of query qn
+    for (int ch = 0; ch < NCH; ++ch) {
+      sc[ch] = floatx4{};
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        sc[ch] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            *reinterpret_cast<const bf16x8*>(sK + ko + 16 * KS * ch + 32 * c), qf[c], sc[ch], 0, 0, 0);
+    }
+    // sc[ch][r]: slot 16 ch + 4 kg + r of query qn
     float m = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      sc[r] = key[r] ? sc[r] * scale_log2 : -INFINITY;
-      m = fmaxf(m, sc[r]);
-    }
+    for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        sc[ch][r] = key[ch][r] ? sc[ch][r] * scale_log2 : -INFINITY;
+        m = fmaxf(m, sc[ch][r]);
+      }
     m = xor32_max(row16_max(m));
-    bf16x4 pb;
+    s16x4 pp[NCH];
     float l = 0.f;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      pb[r] = (bf16)__builtin_amdgcn_exp2f(sc[r] - m);  // 0 where masked
-      l += (float)pb[r];
+    for (int ch = 0; ch < NCH; ++ch) {
+      bf16x4 pb;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        pb[r] = (bf16)__builtin_amdgcn_exp2f(sc[ch][r] - m);  // 0 where masked
+        l += (float)pb[r];
+      }
+      pp[ch] = __builtin_bit_cast(s16x4, pb);
     }
     l = xor32_sum(row16_sum(l));
     const float inv = 1.f / l;
-    const s16x4 pp = __builtin_bit_cast(s16x4, pb);
     // features 16 c .. 16 c + 31 of query qn: 8 consecutive ones per key group
     auto out_chunks = [&](int c) {
       // o0[r], o1[r]: features 16 c + 4 kg + r and 16 (c + 1) + 4 kg + r
-      const floatx4 o0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
-          *reinterpret_cast<const s16x4*>(sV + vo + 16 * VS * c), pp, floatx4{}, 0, 0, 0);
-      const floatx4 o1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
-          *reinterpret_cast<const s16x4*>(sV + vo + 16 * VS * (c + 1)), pp, floatx4{}, 0, 0, 0);
+      floatx4 o0 = {}, o1 = {};
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        o0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+            *reinterpret_cast<const s16x4*>(sV + vo + 16 * VS * c + 16 * ch), pp[ch], o0, 0, 0, 0);
+        o1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+            *reinterpret_cast<const s16x4*>(sV + vo + 16 * VS * (c + 1) + 16 * ch), pp[ch], o1, 0, 0, 0);
+      }
       bf16x4 b0, b1;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -569,6 +421,7 @@ __global__ __launch_bounds__(512) void lg_cross_attn_mfma(const bf16* __restrict
       }
       return u32x4_t{x[0], x[1], y[0], y[1]};
     };
+    const int h = h0 + hl;
     if constexpr (DH % 64 == 0) {
       // Whole 128-byte lines per store: features 16 c .. 16 c + 63 of a
       // query are e0 (first half) and e1 (second half) of its four lanes.
@@ -607,29 +460,46 @@ __global__ __launch_bounds__(512) void lg_cross_attn_mfma(const bf16* __restrict
       }
     }
   };
-  // (group, head) pair k = 16-query group k / H, head k % H: wave w takes
-  // pairs w, w + 8, ..., so the 8 waves work on 8 consecutive pairs at a
-  // time (with 8 heads, the 8 pieces of the same rows); Q of the wave's
+  // (group, head) pair k = 16-query group k / hb, head h0 + k % hb: wave w
+  // takes pairs w, w + 8, ..., so the 8 waves work on 8 consecutive pairs at
+  // a time (with 8 heads, the 8 pieces of the same rows); Q of the wave's
   // next pair requested first
-  const int n_pairs = n_groups * H;
+  const int n_pairs = n_groups * hb;
   for (int k = wave; k < n_pairs; k += 16) {
-    load_q((k + 8) / H, (k + 8) % H, qb);
-    work(k / H, k % H, qa);
+    load_q((k + 8) / hb, h0 + (k + 8) % hb, qb);
+    work(k / hb, k % hb, qa);
     if (k + 8 >= n_pairs) break;
-    load_q((k + 16) / H, (k + 16) % H, qa);
-    work((k + 8) / H, (k + 8) % H, qb);
+    load_q((k + 16) / hb, h0 + (k + 16) % hb, qa);
+    work((k + 8) / hb, (k + 8) % hb, qb);
   }
 }
 
-static bool lg_dot_path(bool bf, int l_local, bool gpool) { return bf && l_local + (gpool ? 1 : 0) <= kLgDotKeys; }
-// the window, started at a multiple of 4, and the pooled token within 16 slots
-static bool lg_mfma_path(bool bf, int l_local, bool gpool, int H) {
-  return bf && l_local + (gpool ? 1 : 0) + 3 <= kLgMfmaSlots && H <= kLgMfmaHeads;
+// slots of the MFMA kernel: the window from its start rounded down to a
+// multiple of 4, and the pooled token (0: the window does not fit)
+static int lg_mfma_slots(bool bf, int l_local, bool gpool) {
+  const int need = l_local + (gpool ? 1 : 0) + 3;
+  return bf && need <= kLgMfmaMaxSlots ? (need + 15) / 16 * 16 : 0;
 }
-bool lg_attention_all_heads(bool bf, int l_local, bool gpool, int H) { return lg_mfma_path(bf, l_local, gpool, H); }
-int lg_attention_q_block(bool bf, int l_local, bool gpool, int H) {
-  if (lg_mfma_path(bf, l_local, gpool, H)) return kLgMfmaTile;
-  return lg_dot_path(bf, l_local, gpool) ? kLgDotTile : kLgQueries;
+static int lg_mfma_max_heads(int ns, int dh) {
+  switch (ns) {
+#define TX_LGH(NS) \
+  case NS: return dh == 32 ? lg_max_heads(NS, 32) : dh == 64 ? lg_max_heads(NS, 64) : lg_max_heads(NS, 128);
+    TX_LGH(16) TX_LGH(32) TX_LGH(48) TX_LGH(64) TX_LGH(80)
+#undef TX_LGH
+    default: return 0;
+  }
+}
+int lg_attention_heads_per_tile(bool bf, int l_local, bool gpool, int H, int dh) {
+  const int ns = lg_mfma_slots(bf, l_local, gpool);
+  if (ns == 0) return 1;
+  int hb = std::min(H, lg_mfma_max_heads(ns, dh));
+  while (H % hb) --hb;
+  return hb;
+}
+int lg_attention_q_block(bool bf, int l_local, bool gpool, int H, int dh) {
+  if (lg_mfma_slots(bf, l_local, gpool) == 0) return kLgQueries;
+  const int hb = lg_attention_heads_per_tile(bf, l_local, gpool, H, dh);
+  return 16 * ((kLgMfmaPairs + hb - 1) / hb);
 }
 
 hipError_t launch_lg_attention(bool bf, const void* q, int ldq, void* out, int ldo, const void* pool,
@@ -638,34 +508,31 @@ hipError_t launch_lg_attention(bool bf, const void* q, int ldq, void* out, int l
                                const void* gkv, int gkv_ld, int dec_layer, hipStream_t s) {
   if (n_tiles <= 0) return hipSuccess;
   if (l_local < 1 || l_local > kMaxLocal) return hipErrorInvalidValue;
-  if (q_block != lg_attention_q_block(bf, l_local, gkv != nullptr, g.H)) return hipErrorInvalidValue;
+  if (g.dh != 32 && g.dh != 64 && g.dh != 128) return hipErrorInvalidValue;
+  const bool gp = gkv != nullptr;
+  if (q_block != lg_attention_q_block(bf, l_local, gp, g.H, g.dh)) return hipErrorInvalidValue;
   const float sl2 = 1.4426950408889634f / sqrtf((float)g.dh);
-  if (lg_mfma_path(bf, l_local, gkv != nullptr, g.H)) {
-#define TX_LGM(DH)                                                                                          \
-  lg_cross_attn_mfma<DH><<<n_tiles, 512, 0, s>>>((const bf16*)q, ldq, (bf16*)out, ldo, (const bf16*)pool,          \
-                                                 page_table, max_pages, g, layer_slot, reqs, tiles, l_local,       \
-                                                 (const bf16*)gkv, gkv_ld, dec_layer, sl2)
-    switch (g.dh) {
-      case 32: TX_LGM(32); break;
-      case 64: TX_LGM(64); break;
-      case 128: TX_LGM(128); break;
-      default: return hipErrorInvalidValue;
-    }
-#undef TX_LGM
-    return hipGetLastError();
+  if (const int ns = lg_mfma_slots(bf, l_local, gp)) {
+    const int hb = lg_attention_heads_per_tile(bf, l_local, gp, g.H, g.dh);
+#define TX_LGM(DH, NS)                                                                                            \
+  lg_cross_attn_mfma<DH, NS><<<n_tiles, 512, 0, s>>>((const bf16*)q, ldq, (bf16*)out, ldo, (const bf16*)pool,        \
+                                                     page_table, max_pages, g, layer_slot, reqs, tiles, l_local, hb, \
+                                                     (const bf16*)gkv, gkv_ld, dec_layer, sl2)
+#define TX_LGM_NS(DH)                 \
+  switch (ns) {                       \
+    case 16: TX_LGM(DH, 16); break;   \
+    case 32: TX_LGM(DH, 32); break;   \
+    case 48: TX_LGM(DH, 48); break;   \
+    case 64: TX_LGM(DH, 64); break;   \
+    default: TX_LGM(DH, 80); break;   \
   }
-  if (lg_dot_path(bf, l_local, gkv != nullptr)) {
-#define TX_LGD(DH)                                                                                             \
-  lg_cross_attn_dot<DH><<<n_tiles, 4 * kLgDotQueries, 0, s>>>((const bf16*)q, ldq, (bf16*)out, ldo, (const bf16*)pool,      \
-                                                page_table, max_pages, g, layer_slot, reqs, tiles, l_local,    \
-                                                (const bf16*)gkv, gkv_ld, dec_layer, sl2)
     switch (g.dh) {
-      case 32: TX_LGD(32); break;
-      case 64: TX_LGD(64); break;
-      case 128: TX_LGD(128); break;
-      default: return hipErrorInvalidValue;
+      case 32: TX_LGM_NS(32); break;
+      case 64: TX_LGM_NS(64); break;
+      default: TX_LGM_NS(128); break;
     }
-#undef TX_LGD
+#undef TX_LGM_NS
+#undef TX_LGM
     return hipGetLastError();
   }
   const size_t lds = (size_t)(l_local + 1) * 4 * (g.dh / 4 + 4) * 2 * sizeof(float);

@@ -218,11 +218,11 @@ hipError_t launch_store_rows(bool bf, const void* src, int W, const PoolReq* req
 // and, when gkv is not null, to the request's global token, whose key and
 // value are columns [2*dec_layer*d + h*dh ..) and [(2*dec_layer+1)*d + h*dh ..)
 // of row `slot` of gkv (row stride gkv_ld). Tiles of q_block =
-// lg_attention_q_block(bf, l_local, gkv != nullptr, H) queries (checked).
-int lg_attention_q_block(bool bf, int l_local, bool gpool, int H);
-// Whether a tile of that kernel serves every head of its queries (tiles
-// planned with one head) rather than one head.
-bool lg_attention_all_heads(bool bf, int l_local, bool gpool, int H);
+// lg_attention_q_block(bf, l_local, gkv != nullptr, H, dh) queries (checked),
+// each serving heads [head * hb, head * hb + hb) of its queries with
+// hb = lg_attention_heads_per_tile(...) (tiles planned with H / hb heads).
+int lg_attention_q_block(bool bf, int l_local, bool gpool, int H, int dh);
+int lg_attention_heads_per_tile(bool bf, int l_local, bool gpool, int H, int dh);
 hipError_t launch_lg_attention(bool bf, const void* q, int ldq, void* out, int ldo, const void* pool,
                                const int32_t* page_table, int max_pages, PageGeom g, int layer_slot,
                                const AttnReq* reqs, const AttnTile* tiles, int n_tiles, int q_block, int l_local,

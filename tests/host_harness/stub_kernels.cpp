@@ -46,12 +46,12 @@ hipError_t launch_lg_attention(bool, const void*, int, void*, int, const void*, 
                                const AttnReq*, const AttnTile*, int, int, int, const void*, int, int, hipStream_t) {
   return hipSuccess;
 }
-int lg_attention_q_block(bool bf, int l_local, bool gpool, int H) {
-  const int k = l_local + (gpool ? 1 : 0);
-  return bf && k <= 13 && H <= 8 ? 288 : bf && k <= 16 ? (1 << 20) : 64;
+int lg_attention_heads_per_tile(bool bf, int l_local, bool gpool, int H, int) {
+  return bf && l_local + (gpool ? 1 : 0) + 3 <= 80 ? (H % 2 ? 1 : 2) : 1;
 }
-bool lg_attention_all_heads(bool bf, int l_local, bool gpool, int H) {
-  return bf && l_local + (gpool ? 1 : 0) <= 13 && H <= 8;
+int lg_attention_q_block(bool bf, int l_local, bool gpool, int H, int dh) {
+  const int hb = lg_attention_heads_per_tile(bf, l_local, gpool, H, dh);
+  return bf ? 16 * ((144 + hb - 1) / hb) : 64;
 }
 bool gemm_ln_ok(int N, int K, int lda, int ldc) { return N % 128 == 0 && K % 64 == 0 && lda % 8 == 0 && ldc % 8 == 0; }
 hipError_t launch_fold_ln_weight(const void*, int, int, const float*, const float*, const float*, void*, float*,

@@ -66,17 +66,22 @@ CASES = [
     ("dh64-L10-pool", ModelConfig(256, 4, 512, 2, 2, rel_pos_buckets=16), 10, True, SHARP, BF16_TOL),
     ("dh128-L64-pool", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16), 64, True, SHARP, BF16_TOL),
     ("dh64-L5-nopool", ModelConfig(256, 4, 512, 2, 1, rel_pos_buckets=0), 5, False, SHARP, BF16_TOL),
-    # bf16 windows of at most 16 keys run on the dot2 kernel, longer ones on
-    # the general kernel: both sides of that boundary, d_head 32, and windows
-    # of 12 and 13 keys with and without the pooled token
+    # bf16 windows run on the MFMA kernel in 16, 32, 48, 64 or 80 slots (the
+    # window from its start rounded down to 4, and the pooled token), with as
+    # many heads per block as its LDS holds: both sides of the 16-slot
+    # boundary (12 and 13 keys with and without the pooled token), every
+    # slot count, d_head 32, 64 and 128
     ("dh32-L12-pool", ModelConfig(64, 2, 256, 1, 2, rel_pos_buckets=8), 12, True, SHARP, BF16_TOL),
     ("dh128-L13-nopool", ModelConfig(256, 2, 1024, 2, 1, rel_pos_buckets=0), 13, False, SHARP, BF16_TOL),
     ("dh64-L13-pool", ModelConfig(256, 4, 512, 2, 2, rel_pos_buckets=16), 13, True, SHARP, BF16_TOL),
     ("dh32-L15-pool", ModelConfig(64, 2, 256, 1, 2, rel_pos_buckets=8), 15, True, SHARP, BF16_TOL),
-    # more heads than the MFMA kernel's blocks serve (8): the dot2 kernel
+    # more heads than an MFMA block serves (8): two head groups per request
     ("dh32-H16-L10-pool", ModelConfig(512, 16, 1024, 1, 2, rel_pos_buckets=8), 10, True, SHARP, BF16_TOL),
     ("dh64-L16-nopool", ModelConfig(256, 4, 512, 2, 1, rel_pos_buckets=0), 16, False, SHARP, BF16_TOL),
     ("dh128-L14-nopool", ModelConfig(256, 2, 1024, 2, 1, rel_pos_buckets=0), 14, False, SHARP, BF16_TOL),
+    ("dh64-L40-pool", ModelConfig(256, 4, 512, 2, 2, rel_pos_buckets=16), 40, True, SHARP, BF16_TOL),
+    ("dh128-L50-nopool", ModelConfig(256, 2, 1024, 2, 1, rel_pos_buckets=0), 50, False, SHARP, BF16_TOL),
+    ("dh32-L64-nopool", ModelConfig(64, 2, 256, 1, 2, rel_pos_buckets=8), 64, False, SHARP, BF16_TOL),
     ("dh128-L16-pool", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16), 16, True, SHARP, BF16_TOL),
 ]
 
@@ -95,14 +100,15 @@ def test_sparse_ragged(oracle_mod, name, model, l_local, pool, variant, tol):
 # Requests with more queries than one tile of the MFMA kernel (288): two
 # full tiles and a partial one, a tile boundary inside the serving tokens,
 # and the serving/candidate split inside a tile; 8 heads, so every wave of a
-# block works (group, head) pairs of its own. The same requests on the dot2
-# kernel (windows of 14 and 15 keys): several passes of 128 queries per
-# request, odd query counts (the last pair of queries half out of the tile).
+# block works (group, head) pairs of its own. The same requests with longer
+# windows, whose blocks serve fewer heads and larger query tiles (576 or 1152
+# queries): two head groups per request, a request in one or two tiles.
 MULTI_TILE = dict(L=[300, 75, 140], S=[40, 300, 7], C=[600, 12, 281])
 MULTI_TILE_CASES = [
-    ("mfma-dh128-H8-L10-pool", ModelConfig(256, 8, 1024, 1, 2, rel_pos_buckets=16), 10, True),
-    ("dot-dh128-L14-pool", ModelConfig(256, 2, 1024, 1, 2, rel_pos_buckets=16), 14, True),
-    ("dot-dh64-L15-nopool", ModelConfig(256, 4, 512, 1, 2, rel_pos_buckets=0), 15, False),
+    ("ns16-dh32-H8-L10-pool", ModelConfig(256, 8, 1024, 1, 2, rel_pos_buckets=16), 10, True),
+    ("ns32-dh128-L14-pool", ModelConfig(256, 2, 1024, 1, 2, rel_pos_buckets=16), 14, True),
+    ("ns32-dh64-L15-nopool", ModelConfig(256, 4, 512, 1, 2, rel_pos_buckets=0), 15, False),
+    ("ns80-dh32-H8-L64-pool", ModelConfig(256, 8, 1024, 1, 2, rel_pos_buckets=16), 64, True),
 ]
 
 
