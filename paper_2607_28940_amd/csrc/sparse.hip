@@ -121,7 +121,7 @@ hipError_t launch_store_rows(bool bf, const void* src, int W, const PoolReq* req
 
 // ---------------------------------------------------------------- attention
 
-// One block per tile of 64 queries of one (request, head): the keys and
+// fp32 models. One block per tile of 64 queries of one (request, head): the keys and
 // values (at most l_local + 1) go to LDS as fp32, sized for the launch's
 // window so that many blocks share a CU (K rows are read feature-fastest, V
 // from the page's transposed, k-permuted layout key-fastest, both
@@ -535,16 +535,17 @@ hipError_t launch_lg_attention(bool bf, const void* q, int ldq, void* out, int l
 #undef TX_LGM
     return hipGetLastError();
   }
+  // fp32 models (every bf16 window has its MFMA slot count)
+  if (bf) return hipErrorInvalidValue;
   const size_t lds = (size_t)(l_local + 1) * 4 * (g.dh / 4 + 4) * 2 * sizeof(float);
-#define TX_LG(TT, DH)                                                                                            \
-  lg_cross_attn<TT, DH><<<n_tiles, 256, lds, s>>>((const TT*)q, ldq, (TT*)out, ldo, (const TT*)pool, page_table, \
-                                                max_pages, g, layer_slot, reqs, tiles, l_local, (const TT*)gkv,  \
-                                                gkv_ld, dec_layer, sl2)
+#define TX_LG(DH)                                                                                                   \
+  lg_cross_attn<float, DH><<<n_tiles, 256, lds, s>>>((const float*)q, ldq, (float*)out, ldo, (const float*)pool,   \
+                                                   page_table, max_pages, g, layer_slot, reqs, tiles, l_local,       \
+                                                   (const float*)gkv, gkv_ld, dec_layer, sl2)
   switch (g.dh) {
-    case 32: if (bf) TX_LG(bf16, 32); else TX_LG(float, 32); break;
-    case 64: if (bf) TX_LG(bf16, 64); else TX_LG(float, 64); break;
-    case 128: if (bf) TX_LG(bf16, 128); else TX_LG(float, 128); break;
-    default: return hipErrorInvalidValue;
+    case 32: TX_LG(32); break;
+    case 64: TX_LG(64); break;
+    default: TX_LG(128); break;
   }
 #undef TX_LG
   return hipGetLastError();
