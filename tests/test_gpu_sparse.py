@@ -82,6 +82,9 @@ CASES = [
     ("dh64-L40-pool", ModelConfig(256, 4, 512, 2, 2, rel_pos_buckets=16), 40, True, SHARP, BF16_TOL),
     ("dh128-L50-nopool", ModelConfig(256, 2, 1024, 2, 1, rel_pos_buckets=0), 50, False, SHARP, BF16_TOL),
     ("dh32-L64-nopool", ModelConfig(64, 2, 256, 1, 2, rel_pos_buckets=8), 64, False, SHARP, BF16_TOL),
+    # 6 heads: all six in one block at 16 slots, three groups of two at 80
+    ("dh64-H6-L10-pool", ModelConfig(384, 6, 1024, 1, 2, rel_pos_buckets=8), 10, True, SHARP, BF16_TOL),
+    ("dh64-H6-L64-pool", ModelConfig(384, 6, 1024, 1, 2, rel_pos_buckets=8), 64, True, SHARP, BF16_TOL),
     ("dh128-L16-pool", ModelConfig(256, 2, 1024, 2, 2, rel_pos_buckets=16), 16, True, SHARP, BF16_TOL),
 ]
 
