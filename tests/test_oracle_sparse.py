@@ -92,6 +92,7 @@ CASES = [
     ("L3-nopool", 3, False, 17, 3, 5, 0),
     ("history-shorter-than-window", 10, True, 6, 2, 4, 0),
     ("S0", 4, True, 20, 0, 5, 0),
+    ("L64-pool-append", 64, True, 150, 3, 4, 5),
 ]
 
 
