@@ -86,21 +86,24 @@ def test_headline_full(oracle_mod):
     torch.cuda.empty_cache()
 
 
-def test_headline_sparse_full(oracle_mod):
+@pytest.mark.parametrize("l_local", [10, 64])
+def test_headline_sparse_full(oracle_mod, l_local):
     """The headline batch with the local-global sparse cross-attention the
     paper's experiments use (Sec. 5 setup: last 10 cached tokens plus an
     attention-pooled global token), in the launch configuration
-    bench.py --l-local 10 times; the oracle recomputes one sampled request."""
+    bench.py --l-local 10 times, and with the longest window (64 tokens: 80
+    key slots, one head per block); the oracle recomputes one sampled
+    request."""
     import dataclasses
     import torch
     wl0 = I.workload("headline")
-    m = dataclasses.replace(wl0.model, l_local=10, global_pool=True)
+    m = dataclasses.replace(wl0.model, l_local=l_local, global_pool=True)
     wl = dataclasses.replace(wl0, model=m)
     w = I.make_weights(m, VARIANT)
-    log("headline sparse: building 256 caches")
+    log(f"headline sparse L{l_local}: building 256 caches")
     run = DeviceCase(wl, w)
     _build_all(run, 128)
-    _check_sampled(run, oracle_mod.Oracle(m, w), [77], "headline sparse")
+    _check_sampled(run, oracle_mod.Oracle(m, w), [77], f"headline sparse L{l_local}")
     torch.cuda.empty_cache()
 
 
